@@ -1,0 +1,236 @@
+"""Benchmark: MoE expert layer forward+backward on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input, all through
+the C ABI on one stream: route -> permute -> grouped SwiGLU forward ->
+combine -> combine backward -> grouped SwiGLU backward (data and weight
+gradients) -> permutation backward.  Inputs are resident in HBM before the
+timed region starts.
+
+Prints ONE JSON line (rank 0).  Default workload: T=4096 tokens, d=2048,
+E=64 experts, top-6, f=1408 SwiGLU (bf16, fp32 router, seed 0).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+METRIC = "MoE layer fwd+bwd tokens/s and grouped-GEMM TFLOP/s (% bf16 MFMA peak)"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+GEMM_KERNELS = ("gemm_fwd_gate_up", "gemm_fwd_down", "gemm_dgrad_down", "gemm_dgrad_gate_up",
+                "gemm_wgrad_gate_up", "gemm_wgrad_down")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Layer:
+    """Preallocated buffers and one fwd+bwd step through the C ABI."""
+
+    def __init__(self, wl: W.Workload, inp: dict):
+        from paper_2607_01844_amd import moe
+        self.moe, self.wl, self.inp = moe, wl, inp
+        dev = inp["x"].device
+        T, k, d, f, E_loc = wl.T, wl.k, wl.d, wl.f, wl.E_loc
+        cap = wl.cap
+        bf = torch.bfloat16
+        e = lambda *s, dt=bf: torch.empty(s, dtype=dt, device=dev)  # noqa: E731
+        self.idx, self.gate = e(T, k, dt=torch.int32), e(T, k, dt=torch.float32)
+        self.logits = e(T, wl.E, dt=torch.float32)
+        self.hg, self.hu, self.yp = e(cap, f), e(cap, f), e(cap, d)
+        self.y, self.dyp, self.dgate = e(T, d), e(cap, d), e(T, k, dt=torch.float32)
+        self.dxp, self.dx = e(cap, d), e(T, d)
+        self.dwg, self.dwu = torch.empty_like(inp["w_gate"]), torch.empty_like(inp["w_up"])
+        self.dwd = torch.empty_like(inp["w_down"])
+        self.pm = None
+
+    def step(self):
+        m, wl, inp = self.moe, self.wl, self.inp
+        m.moe_route(inp["x"], inp["w_router"], inp["router_bias"], wl.k, wl.renorm,
+                    logits=self.logits, topk_idx=self.idx, topk_gate=self.gate)
+        pm = m.moe_permute(inp["x"], self.idx, wl.E, wl.expert_begin, wl.E_loc) \
+            if self.pm is None else self._permute_into()
+        self.pm = pm
+        off = pm["expert_offsets"]
+        m.moe_grouped_swiglu_fwd(pm["x_perm"], off, inp["w_gate"], inp["w_up"], inp["w_down"],
+                                 cap=wl.cap, h_gate=self.hg, h_up=self.hu, y_perm=self.yp)
+        m.moe_combine(self.yp, pm["dst"], self.gate, out=self.y)
+        m.moe_combine_bwd(inp["dy"], self.yp, pm["dst"], self.gate, dy_perm=self.dyp,
+                          dgate=self.dgate)
+        m.moe_grouped_swiglu_bwd(self.dyp, pm["x_perm"], self.hg, self.hu, off, inp["w_gate"],
+                                 inp["w_up"], inp["w_down"], cap=wl.cap, dx_perm=self.dxp,
+                                 dw_gate=self.dwg, dw_up=self.dwu, dw_down=self.dwd)
+        m.moe_combine(self.dxp, pm["dst"], None, out=self.dx)
+
+    def _permute_into(self):
+        # reuse the permutation buffers of the first step (no allocation)
+        m, wl, inp, pm = self.moe, self.wl, self.inp, self.pm
+        import ctypes
+        n = ctypes.c_size_t()
+        m._check(m.lib.moe_permute_workspace_bytes(wl.T, wl.E, wl.k, wl.E_loc, ctypes.byref(n)),
+                 "moe_permute_workspace_bytes")
+        ws = m.workspace(n.value, inp["x"].device, "permute")
+        m._check(m.lib.moe_permute(m._ptr(inp["x"]), m._ptr(self.idx), wl.T, wl.d, wl.E, wl.k,
+                                   wl.expert_begin, wl.E_loc, m._ptr(pm["expert_offsets"]),
+                                   m._ptr(pm["counts_global"]), m._ptr(pm["row_src"]),
+                                   m._ptr(pm["dst"]), m._ptr(pm["x_perm"]), m._ptr(ws),
+                                   ws.numel(), m._stream()), "moe_permute")
+        return pm
+
+
+def kernel_table(wl, M, T_touched, prof, steps):
+    """Per-kernel average time and algorithmic work per launch."""
+    d, f, T, k = wl.d, wl.f, wl.T, wl.k
+    flops = {"gemm_fwd_gate_up": 4.0 * M * d * f, "gemm_fwd_down": 2.0 * M * d * f,
+             "gemm_dgrad_down": 2.0 * M * d * f, "gemm_dgrad_gate_up": 4.0 * M * d * f,
+             "gemm_wgrad_gate_up": 4.0 * M * d * f, "gemm_wgrad_down": 2.0 * M * d * f,
+             "route_logits": 2.0 * T * d * wl.E}
+    # combine runs twice per step (weighted forward, unit-weight permute backward)
+    comb = 0.5 * ((M * d * 2 + T * d * 2 + T * k * 8) + (M * d * 2 + T * d * 2 + T * k * 4))
+    bytes_ = {"permute_gather": T_touched * d * 2 + M * d * 2 + T * k * 4,
+              "combine": comb,
+              "combine_bwd": T * d * 2 + 2 * M * d * 2 + T * k * 12}
+    rows = {}
+    for name, (ms, n) in prof.items():
+        avg_ms = ms / n
+        r = {"avg_us": round(avg_ms * 1e3, 2), "launches_per_step": n / steps}
+        if name in flops:
+            r["tflops"] = round(flops[name] / (avg_ms * 1e-3) / 1e12, 1)
+            if name.startswith("gemm"):
+                r["frac_bf16_peak"] = round(r["tflops"] / PEAK_BF16_TFLOPS, 3)
+        if name in bytes_:
+            r["gbs"] = round(bytes_[name] / (avg_ms * 1e-3) / 1e9, 1)
+            r["frac_hbm_peak"] = round(r["gbs"] / PEAK_HBM_GBS, 3)
+        rows[name] = r
+    return rows, flops, bytes_
+
+
+def cpu_baseline(wl, inp, budget_s: float):
+    """The oracle (as is) on the first T_s tokens of the same workload."""
+    import oracle
+    h = {"x": W.bf16_bits(inp["x"]), "w_r": inp["w_router"].cpu().numpy(),
+         "bias": None if inp["router_bias"] is None else inp["router_bias"].cpu().numpy(),
+         "wg": W.bf16_bits(inp["w_gate"]), "wu": W.bf16_bits(inp["w_up"]),
+         "wd": W.bf16_bits(inp["w_down"]), "dy": W.bf16_bits(inp["dy"])}
+
+    def run(ts):
+        t0 = time.perf_counter()
+        oracle.layer(h["x"][:ts], h["w_r"], h["bias"], h["wg"], h["wu"], h["wd"], h["dy"][:ts],
+                     wl.k, e_begin=wl.expert_begin, E_loc=wl.E_loc, renorm=wl.renorm,
+                     prec="f32")
+        return time.perf_counter() - t0
+
+    probe_t = 32
+    dt = run(probe_t)
+    ts = int(min(wl.T, max(probe_t, probe_t * budget_s / max(dt, 1e-3))))
+    dt = run(ts)
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(ts / dt, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp32 oracle fwd+bwd (routing, permutation, expert FFN, combine, all "
+                      f"gradients) on the first {ts} of {wl.T} tokens with the full expert "
+                      f"weights; {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mid", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = W.WORKLOADS[args.workload]
+    log(f"[bench] workload {wl.describe()}")
+    inp = W.make_inputs(wl, seed=0, device="cuda")
+    layer = Layer(wl, inp)
+    for _ in range(args.warmup):
+        layer.step()
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        layer.step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    tok_s = wl.T / (ms * 1e-3)
+    log(f"[bench] {ms:.3f} ms/step, {tok_s:.0f} tokens/s")
+
+    off = layer.pm["expert_offsets"].cpu().numpy()
+    M = int(off[-1])
+    cnt = np.diff(off)
+    dst = layer.pm["dst"].cpu().numpy()
+    T_touched = int((dst >= 0).any(1).sum())
+
+    kernels, gemm_tflops, roof = {}, None, None
+    if not args.no_kernel_timing:
+        m = layer.moe
+        m.profile_reset()
+        m.profile_enable(True)
+        for _ in range(args.steps):
+            layer.step()
+        torch.cuda.synchronize()
+        m.profile_enable(False)
+        prof = m.profile_query()
+        m.profile_reset()
+        kernels, flops, _ = kernel_table(wl, M, T_touched, prof, args.steps)
+        gemm_ms = sum(prof[n][0] for n in GEMM_KERNELS if n in prof) / args.steps
+        gemm_tflops = 18.0 * M * wl.d * wl.f / (gemm_ms * 1e-3) / 1e12
+        dom = max((n for n in GEMM_KERNELS if n in prof), key=lambda n: prof[n][0])
+        avg_s = prof[dom][0] / prof[dom][1] * 1e-3
+        ach = flops[dom] / avg_s / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "avg_us": round(avg_s * 1e6, 2),
+                "work_per_launch": f"{flops[dom]:.4g} FLOP"}
+        log(f"[bench] grouped GEMMs {gemm_tflops:.0f} TFLOP/s; dominant {dom} {ach:.0f} TFLOP/s")
+
+    cpu = None
+    if args.cpu_budget > 0:
+        log("[bench] cpu baseline ...")
+        cpu = cpu_baseline(wl, inp, args.cpu_budget)
+        log(f"[bench] cpu baseline {cpu['value']} tokens/s")
+
+    out = {
+        "metric": METRIC, "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; random-init weights)",
+        "config": {**wl.describe(), "M": M, "tokens_with_local_slot": T_touched,
+                   "load": W.load_stats(cnt)},
+        "grouped_gemm_tflops": None if gemm_tflops is None else round(gemm_tflops, 1),
+        "grouped_gemm_frac_bf16_peak": None if gemm_tflops is None
+        else round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "device": torch.cuda.get_device_name(0),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

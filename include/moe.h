@@ -1,0 +1,194 @@
+/*
+ * moe.h - C ABI of the MI355X (gfx950) MoE expert-layer library.
+ *
+ * The layer is the Mixture-of-Experts feed-forward block of
+ * Mixture-of-Parallelisms (Sec. 2.1, "Mixture-of-Experts": a light router
+ * sends every token to its top-k of E experts; Sec. 3.1: H = d model width,
+ * I = f expert width, k routing degree, N = T tokens on the device; eq.
+ * (peaks): the N k H routed activations and the N_r I expert intermediates),
+ * on one GPU's expert-parallel share (Sec. 3.2, hybrid expert parallelism:
+ * this device owns experts [expert_begin, expert_begin + num_local)).
+ * Sec. 3.3 (LLEP) moves where token-expert products run, never which ones
+ * run, so the calls below compute exactly the plain layer.
+ *
+ * Conventions shared by every call
+ *  - bf16 values are raw IEEE bfloat16 bit patterns (moe_bf16); fp32->bf16 is
+ *    round-to-nearest-even.  All arrays are dense and row-major.
+ *  - Every pointer is DEVICE memory owned by the caller; the library
+ *    allocates nothing and keeps no reference after the call returns.
+ *    Required pointers must be non-NULL and 16-byte aligned.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *    Calls only enqueue work and return; no call synchronises the device.
+ *    Data-dependent sizes (M, the number of local assignments) stay on the
+ *    device: kernels read them from expert_offsets[num_local].
+ *  - Return value: MOE_OK or a negative moe_status.  Arguments are checked
+ *    on the host before any HIP call; on MOE_ERR_INVALID_ARG or
+ *    MOE_ERR_WORKSPACE nothing was enqueued and outputs are untouched.
+ *    moe_last_error() returns a message for the calling thread's last error.
+ *  - Outputs must not alias inputs.  Results are bitwise deterministic run to
+ *    run (no floating-point atomics).
+ *  - cap >= T * min(k, num_local) is the row capacity of permuted buffers;
+ *    rows [M, cap) of them are never read and are left unspecified.
+ *  - Limits: 1 <= k <= MOE_MAX_K, k <= E <= MOE_MAX_E, T >= 0,
+ *    T * k < 2^31, d and f multiples of 8 and >= 8.
+ *  - Device-side garbage (an expert id outside [0, E) in a caller-supplied
+ *    topk_idx) is undefined behaviour.
+ */
+#ifndef MOE_MI355X_H
+#define MOE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+#define MOE_MAX_K 16
+#define MOE_MAX_E 1024
+
+typedef uint16_t moe_bf16;
+
+enum moe_status {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1,
+  MOE_ERR_UNSUPPORTED = -2,
+  MOE_ERR_WORKSPACE = -3,
+  MOE_ERR_HIP = -4
+};
+
+/* flags of moe_grouped_swiglu_bwd */
+enum { MOE_BWD_DGRAD = 1, MOE_BWD_WGRAD = 2 };
+
+int moe_abi_version(void);
+const char* moe_status_string(int status);
+const char* moe_last_error(void);
+
+/* ------------------------------------------------------------------ router
+ * Router scores and top-k selection (Sec. 2.1: each token goes to its top-k
+ * experts; the router is a dense weight, Sec. 3.1 eq. (param-decomp)).
+ *
+ * logits[t][e] = fp32 fused-multiply-add chain over j = 0..d-1 ascending of
+ *   float(x[t][j]) * w_router[j][e], started at +0.0f, then + router_bias[e]
+ *   (one fp32 add; bias optional).  This order is fixed so that routing is
+ *   reproducible bit for bit on any device.
+ * topk_idx[t][i], i = 0..k-1: the k experts with the largest logits, taken in
+ *   the total order (logit descending, expert index ascending); -0.0 and +0.0
+ *   are equal.  Slot i holds the i-th in that order.
+ * topk_gate[t][i]: renorm = 0 -> softmax over all E logits, evaluated at the
+ *   chosen expert; renorm = 1 -> softmax over the k chosen logits.
+ *
+ * x [T][d] bf16; w_router [d][E] fp32; router_bias [E] fp32 or NULL;
+ * topk_idx [T][k] int32; topk_gate [T][k] fp32; logits [T][E] fp32 or NULL.
+ * When logits is NULL the workspace must hold moe_route_workspace_bytes().
+ * Logits must be finite (NaN routing is unspecified).
+ */
+int moe_route_workspace_bytes(int64_t T, int E, size_t* bytes);
+int moe_route(const moe_bf16* x, const float* w_router, const float* router_bias, int64_t T,
+              int d, int E, int k, int renorm, int32_t* topk_idx, float* topk_gate,
+              float* logits, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------- permutation
+ * Group this device's token-expert assignments into contiguous per-expert
+ * segments (the N_r routed rows of Sec. 3.1 eq. (peaks)).
+ *
+ * Assignment a = t*k + i is local when expert_begin <= topk_idx[t][i] <
+ *   expert_begin + num_local; its local expert is e' = topk_idx - expert_begin.
+ * expert_offsets [num_local+1]: exclusive prefix sum of the per-expert
+ *   counts; expert_offsets[num_local] = M.
+ * counts_global [E] (optional): count of every expert over all assignments.
+ * Rows of segment e' hold that expert's assignments in ascending a (a stable
+ *   counting sort): row_src[p] = a for p < M; dst[a] = p, or -1 if a is not
+ *   local.  x_perm[p][:] = x[row_src[p] / k][:] (a bit copy).
+ *
+ * x [T][d] bf16; topk_idx [T][k] int32; row_src [cap] int32; dst [T*k] int32;
+ * x_perm [cap][d] bf16; workspace of moe_permute_workspace_bytes().
+ * T = 0 is valid: offsets become zero.
+ */
+int moe_permute_workspace_bytes(int64_t T, int E, int k, int num_local, size_t* bytes);
+int moe_permute(const moe_bf16* x, const int32_t* topk_idx, int64_t T, int d, int E, int k,
+                int expert_begin, int num_local, int32_t* expert_offsets,
+                int32_t* counts_global, int32_t* row_src, int32_t* dst, moe_bf16* x_perm,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ----------------------------------------------------- grouped SwiGLU FFN
+ * Expert feed-forward on the permuted rows (Sec. 3.1: Theta_exp = Theta(LEHI)
+ * expert weights, N_r I intermediates).  For each local expert e and each row
+ * p of its segment [expert_offsets[e], expert_offsets[e+1]):
+ *   h_gate[p] = x_perm[p] W_gate[e],  h_up[p] = x_perm[p] W_up[e]
+ *   a[p] = silu(h_gate[p]) * h_up[p],  silu(z) = z / (1 + exp(-z))
+ *   y_perm[p] = a[p] W_down[e]
+ * bf16 operands, fp32 accumulation, bf16 results (h_gate, h_up are saved for
+ * the backward; a is computed from the rounded h_gate, h_up).  Experts with no
+ * rows cost nothing; no padding to a capacity.
+ *
+ * w_gate, w_up [num_local][d][f]; w_down [num_local][f][d];
+ * x_perm [cap][d]; h_gate, h_up [cap][f]; y_perm [cap][d]; all bf16.
+ * expert_offsets [num_local+1] as produced by moe_permute.
+ * Workspace: moe_grouped_swiglu_workspace_bytes(cap, num_local, d, f, 0).
+ */
+int moe_grouped_swiglu_workspace_bytes(int64_t cap, int num_local, int d, int f,
+                                       unsigned flags, size_t* bytes);
+int moe_grouped_swiglu_fwd(const moe_bf16* x_perm, const int32_t* expert_offsets, int num_local,
+                           int64_t cap, int d, int f, const moe_bf16* w_gate,
+                           const moe_bf16* w_up, const moe_bf16* w_down, moe_bf16* h_gate,
+                           moe_bf16* h_up, moe_bf16* y_perm, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* Backward of the expert FFN, given dy_perm = dL/dy_perm:
+ *   dA = dy_perm W_down[e]^T
+ *   dh_gate = dA * h_up * silu'(h_gate),  silu'(z) = s (1 + z (1 - s)), s = sigmoid(z)
+ *   dh_up = dA * silu(h_gate)
+ * flags & MOE_BWD_DGRAD: dx_perm = dh_gate W_gate[e]^T + dh_up W_up[e]^T
+ * flags & MOE_BWD_WGRAD: dw_gate[e] = x_perm_e^T dh_gate_e,
+ *   dw_up[e] = x_perm_e^T dh_up_e, dw_down[e] = a_e^T dy_perm_e (sums over the
+ *   rows of expert e); written (not accumulated) as bf16; an expert with no
+ *   rows gets exact zeros.  dh_gate, dh_up and a are rounded to bf16.
+ * dy_perm, x_perm [cap][d]; h_gate, h_up [cap][f]; dx_perm [cap][d];
+ * dw_gate, dw_up [num_local][d][f]; dw_down [num_local][f][d]; all bf16.
+ * Workspace: moe_grouped_swiglu_workspace_bytes(cap, num_local, d, f, flags).
+ */
+int moe_grouped_swiglu_bwd(const moe_bf16* dy_perm, const moe_bf16* x_perm,
+                           const moe_bf16* h_gate, const moe_bf16* h_up,
+                           const int32_t* expert_offsets, int num_local, int64_t cap, int d,
+                           int f, const moe_bf16* w_gate, const moe_bf16* w_up,
+                           const moe_bf16* w_down, moe_bf16* dx_perm, moe_bf16* dw_gate,
+                           moe_bf16* dw_up, moe_bf16* dw_down, unsigned flags, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* ----------------------------------------------------------------- combine
+ * Weighted combination of the expert outputs (Sec. 2.1):
+ *   out[t] = sum over slots i = 0..k-1 ascending with dst[t*k+i] >= 0 of
+ *            topk_gate[t][i] * y_perm[dst[t*k+i]]      (fp32 sum, bf16 result)
+ * A token with no local slot gets 0.  topk_gate = NULL means weight 1; with
+ * it this call is the backward of moe_permute (dx = sum of dx_perm rows).
+ * y_perm [cap][d] bf16; dst [T*k] int32; topk_gate [T][k] fp32; out [T][d].
+ */
+int moe_combine(const moe_bf16* y_perm, const int32_t* dst, const float* topk_gate, int64_t T,
+                int d, int k, moe_bf16* out, void* stream);
+
+/* Backward of moe_combine, given dout = dL/dout:
+ *   dy_perm[dst[t*k+i]] = topk_gate[t][i] * dout[t]          (bf16)
+ *   dgate[t][i] = sum_j dout[t][j] * y_perm[dst[t*k+i]][j]   (fp32; 0 if not local)
+ * dout [T][d] bf16; dy_perm [cap][d] bf16; dgate [T][k] fp32 or NULL.
+ */
+int moe_combine_bwd(const moe_bf16* dout, const moe_bf16* y_perm, const int32_t* dst,
+                    const float* topk_gate, int64_t T, int d, int k, moe_bf16* dy_perm,
+                    float* dgate, void* stream);
+
+/* ------------------------------------------------------------- profiling
+ * Optional per-kernel timing with HIP events recorded on the launch stream
+ * around every kernel the library enqueues (for measurement only; off by
+ * default).  moe_profile_query synchronises on the recorded events.
+ */
+int moe_profile_enable(int on);
+int moe_profile_reset(void);
+int moe_profile_num_kernels(void);
+const char* moe_profile_kernel_name(int id);
+int moe_profile_query(int id, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_MI355X_H */

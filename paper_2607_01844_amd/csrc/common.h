@@ -1,0 +1,119 @@
+// Internal helpers shared by the HIP kernels of the MoE library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "moe.h"
+
+namespace moe {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------ bf16 helpers
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v) << 16);
+}
+
+// fp32 -> bf16 bits, round to nearest even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// ------------------------------------------------------------ wave helpers
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// Compile-time loop: f(std::integral_constant<int, 0..N-1>) (keeps register
+// arrays indexed by constants, so they never fall back to scratch memory).
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// ------------------------------------------------------------ math helpers
+__device__ __forceinline__ float sigmoidf_fast(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+// --------------------------------------------------------- launch plumbing
+struct LaunchCtx {
+  hipStream_t stream;
+};
+
+// Kernel ids for the optional profiler (order = moe_profile_kernel_name).
+enum KernelId {
+  K_ROUTE_LOGITS = 0,
+  K_ROUTE_TOPK,
+  K_PERM_COUNT,
+  K_PERM_SCAN,
+  K_PERM_RANK,
+  K_PERM_GATHER,
+  K_GEMM_SCHED,
+  K_GEMM_FWD_GATE_UP,
+  K_GEMM_FWD_DOWN,
+  K_GEMM_DGRAD_DOWN,
+  K_GEMM_DGRAD_GATE_UP,
+  K_GEMM_WGRAD_GATE_UP,
+  K_GEMM_WGRAD_DOWN,
+  K_COMBINE,
+  K_COMBINE_BWD,
+  K_NUM
+};
+
+// Profiler hooks (no-ops unless moe_profile_enable(1) was called).
+void prof_begin(int id, hipStream_t s);
+void prof_end(int id, hipStream_t s);
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ------------------------------------------------------ kernel launchers
+// (defined next to their kernels; arguments were validated by the C ABI)
+hipError_t launch_route(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
+                        int E, int k, int renorm, int32_t* idx, float* gate, float* logits,
+                        hipStream_t s);
+size_t permute_ws_bytes(int64_t T, int E, int k, int E_loc);
+hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int d, int E, int k,
+                          int e_begin, int E_loc, int32_t* offsets, int32_t* counts_global,
+                          int32_t* row_src, int32_t* dst, uint16_t* x_perm, void* ws,
+                          hipStream_t s);
+hipError_t launch_combine(const uint16_t* y, const int32_t* dst, const float* gate, int64_t T,
+                          int d, int k, uint16_t* out, hipStream_t s);
+hipError_t launch_combine_bwd(const uint16_t* dout, const uint16_t* y, const int32_t* dst,
+                              const float* gate, int64_t T, int d, int k, uint16_t* dy_perm,
+                              float* dgate, hipStream_t s);
+size_t gemm_ws_bytes(int64_t cap, int E_loc, int d, int f, unsigned flags);
+hipError_t launch_ffn_fwd(const uint16_t* x_perm, const int32_t* offsets, int E_loc, int64_t cap,
+                          int d, int f, const uint16_t* wg, const uint16_t* wu,
+                          const uint16_t* wd, uint16_t* hg, uint16_t* hu, uint16_t* y,
+                          void* ws, hipStream_t s);
+hipError_t launch_ffn_bwd(const uint16_t* dy, const uint16_t* x_perm, const uint16_t* hg,
+                          const uint16_t* hu, const int32_t* offsets, int E_loc, int64_t cap,
+                          int d, int f, const uint16_t* wg, const uint16_t* wu,
+                          const uint16_t* wd, uint16_t* dx, uint16_t* dwg, uint16_t* dwu,
+                          uint16_t* dwd, unsigned flags, void* ws, hipStream_t s);
+
+}  // namespace moe

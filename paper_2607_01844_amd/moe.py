@@ -1,0 +1,320 @@
+"""Thin Python binding of libmoe.so (the MI355X MoE expert-layer library).
+
+Every function has the name of the C entry point it calls and only marshals
+arguments: it checks dtype/device/contiguity, allocates outputs and
+workspaces with torch (device memory), and passes raw pointers plus the
+current HIP stream.  All arithmetic runs in the library's HIP kernels.  If
+the library is not built this module raises on import; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmoe.so")
+
+MOE_OK = 0
+MOE_BWD_DGRAD = 1
+MOE_BWD_WGRAD = 2
+MOE_MAX_K = 16
+MOE_MAX_E = 1024
+
+C_SYMBOLS = (
+    "moe_abi_version", "moe_status_string", "moe_last_error",
+    "moe_route_workspace_bytes", "moe_route",
+    "moe_permute_workspace_bytes", "moe_permute",
+    "moe_grouped_swiglu_workspace_bytes", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
+    "moe_combine", "moe_combine_bwd",
+    "moe_profile_enable", "moe_profile_reset", "moe_profile_num_kernels",
+    "moe_profile_kernel_name", "moe_profile_query",
+)
+
+
+class MoEError(RuntimeError):
+    pass
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2607_01844_amd.build` "
+            "(there is no CPU fallback)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, I64, U, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint, ctypes.c_size_t
+    PSZ = ctypes.POINTER(ctypes.c_size_t)
+    sig = {
+        "moe_abi_version": ([], I),
+        "moe_status_string": ([I], ctypes.c_char_p),
+        "moe_last_error": ([], ctypes.c_char_p),
+        "moe_route_workspace_bytes": ([I64, I, PSZ], I),
+        "moe_route": ([P, P, P, I64, I, I, I, I, P, P, P, P, SZ, P], I),
+        "moe_permute_workspace_bytes": ([I64, I, I, I, PSZ], I),
+        "moe_permute": ([P, P, I64, I, I, I, I, I, P, P, P, P, P, P, SZ, P], I),
+        "moe_grouped_swiglu_workspace_bytes": ([I64, I, I, I, U, PSZ], I),
+        "moe_grouped_swiglu_fwd": ([P, P, I, I64, I, I, P, P, P, P, P, P, P, SZ, P], I),
+        "moe_grouped_swiglu_bwd": ([P, P, P, P, P, I, I64, I, I, P, P, P, P, P, P, P, U, P, SZ,
+                                    P], I),
+        "moe_combine": ([P, P, P, I64, I, I, P, P], I),
+        "moe_combine_bwd": ([P, P, P, P, I64, I, I, P, P, P], I),
+        "moe_profile_enable": ([I], I),
+        "moe_profile_reset": ([], I),
+        "moe_profile_num_kernels": ([], I),
+        "moe_profile_kernel_name": ([I], ctypes.c_char_p),
+        "moe_profile_query": ([I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
+                              I),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    return L
+
+
+lib = _load()
+
+
+def _check(status: int, fn: str):
+    if status != MOE_OK:
+        msg = lib.moe_last_error().decode()
+        raise MoEError(f"{fn} -> {lib.moe_status_string(status).decode()}: {msg}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t, dtype, name, dim=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dim is not None and t.dim() != dim:
+        raise ValueError(f"{name}: expected {dim} dims, got {t.dim()}")
+    return t
+
+
+_ws_cache: dict = {}
+
+
+def workspace(nbytes: int, device, tag: str) -> torch.Tensor:
+    """A cached device scratch buffer of at least nbytes (per device and tag)."""
+    key = (str(device), tag)
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
+    return buf
+
+
+# ---------------------------------------------------------------- router
+def moe_route(x, w_router, router_bias, k, renorm=0, logits=None, topk_idx=None, topk_gate=None):
+    """Returns (topk_idx [T,k] int32, topk_gate [T,k] fp32)."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(w_router, torch.float32, "w_router", 2)
+    if router_bias is not None:
+        _need(router_bias, torch.float32, "router_bias", 1)
+    T, d = x.shape
+    E = w_router.shape[1]
+    dev = x.device
+    if topk_idx is None:
+        topk_idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    if topk_gate is None:
+        topk_gate = torch.empty((T, k), dtype=torch.float32, device=dev)
+    ws, nws = None, 0
+    if logits is None:
+        n = ctypes.c_size_t()
+        _check(lib.moe_route_workspace_bytes(T, E, ctypes.byref(n)), "moe_route_workspace_bytes")
+        ws = workspace(n.value, dev, "route")
+        nws = ws.numel()
+    else:
+        _need(logits, torch.float32, "logits", 2)
+    _check(lib.moe_route(_ptr(x), _ptr(w_router), _ptr(router_bias), T, d, E, k, renorm,
+                         _ptr(topk_idx), _ptr(topk_gate), _ptr(logits), _ptr(ws), nws, _stream()),
+           "moe_route")
+    return topk_idx, topk_gate
+
+
+# ------------------------------------------------------------ permutation
+def moe_permute(x, topk_idx, E, expert_begin=0, num_local=None, cap=None, counts_global=True):
+    """Returns dict(expert_offsets, counts_global, row_src, dst, x_perm)."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(topk_idx, torch.int32, "topk_idx", 2)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    num_local = E if num_local is None else num_local
+    cap = T * min(k, num_local) if cap is None else cap
+    dev = x.device
+    offsets = torch.empty(num_local + 1, dtype=torch.int32, device=dev)
+    cg = torch.empty(E, dtype=torch.int32, device=dev) if counts_global else None
+    row_src = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    dst = torch.empty(max(T * k, 1), dtype=torch.int32, device=dev)
+    x_perm = torch.empty((max(cap, 1), d), dtype=torch.bfloat16, device=dev)
+    n = ctypes.c_size_t()
+    _check(lib.moe_permute_workspace_bytes(T, E, k, num_local, ctypes.byref(n)),
+           "moe_permute_workspace_bytes")
+    ws = workspace(n.value, dev, "permute")
+    _check(lib.moe_permute(_ptr(x), _ptr(topk_idx), T, d, E, k, expert_begin, num_local,
+                           _ptr(offsets), _ptr(cg), _ptr(row_src), _ptr(dst), _ptr(x_perm),
+                           _ptr(ws), ws.numel(), _stream()), "moe_permute")
+    return {"expert_offsets": offsets, "counts_global": cg, "row_src": row_src,
+            "dst": dst[: T * k].view(T, k), "x_perm": x_perm, "cap": cap}
+
+
+# ----------------------------------------------------- grouped SwiGLU FFN
+def moe_grouped_swiglu_fwd(x_perm, expert_offsets, w_gate, w_up, w_down, cap=None,
+                           h_gate=None, h_up=None, y_perm=None):
+    """Returns (h_gate, h_up, y_perm), each with cap rows."""
+    _need(x_perm, torch.bfloat16, "x_perm", 2)
+    _need(expert_offsets, torch.int32, "expert_offsets", 1)
+    for n_, t in (("w_gate", w_gate), ("w_up", w_up), ("w_down", w_down)):
+        _need(t, torch.bfloat16, n_, 3)
+    E_loc, d, f = w_gate.shape
+    cap = x_perm.shape[0] if cap is None else cap
+    dev = x_perm.device
+    if h_gate is None:
+        h_gate = torch.empty((max(cap, 1), f), dtype=torch.bfloat16, device=dev)
+    if h_up is None:
+        h_up = torch.empty((max(cap, 1), f), dtype=torch.bfloat16, device=dev)
+    if y_perm is None:
+        y_perm = torch.empty((max(cap, 1), d), dtype=torch.bfloat16, device=dev)
+    n = ctypes.c_size_t()
+    _check(lib.moe_grouped_swiglu_workspace_bytes(cap, E_loc, d, f, 0, ctypes.byref(n)),
+           "moe_grouped_swiglu_workspace_bytes")
+    ws = workspace(n.value, dev, "ffn")
+    _check(lib.moe_grouped_swiglu_fwd(_ptr(x_perm), _ptr(expert_offsets), E_loc, cap, d, f,
+                                      _ptr(w_gate), _ptr(w_up), _ptr(w_down), _ptr(h_gate),
+                                      _ptr(h_up), _ptr(y_perm), _ptr(ws), ws.numel(), _stream()),
+           "moe_grouped_swiglu_fwd")
+    return h_gate, h_up, y_perm
+
+
+def moe_grouped_swiglu_bwd(dy_perm, x_perm, h_gate, h_up, expert_offsets, w_gate, w_up, w_down,
+                           flags=MOE_BWD_DGRAD | MOE_BWD_WGRAD, cap=None, dx_perm=None,
+                           dw_gate=None, dw_up=None, dw_down=None):
+    """Returns (dx_perm or None, dw_gate, dw_up, dw_down or None)."""
+    for n_, t in (("dy_perm", dy_perm), ("x_perm", x_perm), ("h_gate", h_gate), ("h_up", h_up)):
+        _need(t, torch.bfloat16, n_, 2)
+    _need(expert_offsets, torch.int32, "expert_offsets", 1)
+    for n_, t in (("w_gate", w_gate), ("w_up", w_up), ("w_down", w_down)):
+        _need(t, torch.bfloat16, n_, 3)
+    E_loc, d, f = w_gate.shape
+    cap = x_perm.shape[0] if cap is None else cap
+    dev = x_perm.device
+    if flags & MOE_BWD_DGRAD and dx_perm is None:
+        dx_perm = torch.empty((max(cap, 1), d), dtype=torch.bfloat16, device=dev)
+    if flags & MOE_BWD_WGRAD:
+        if dw_gate is None:
+            dw_gate = torch.empty_like(w_gate)
+        if dw_up is None:
+            dw_up = torch.empty_like(w_up)
+        if dw_down is None:
+            dw_down = torch.empty_like(w_down)
+    n = ctypes.c_size_t()
+    _check(lib.moe_grouped_swiglu_workspace_bytes(cap, E_loc, d, f, flags, ctypes.byref(n)),
+           "moe_grouped_swiglu_workspace_bytes")
+    ws = workspace(n.value, dev, "ffn")
+    _check(lib.moe_grouped_swiglu_bwd(_ptr(dy_perm), _ptr(x_perm), _ptr(h_gate), _ptr(h_up),
+                                      _ptr(expert_offsets), E_loc, cap, d, f, _ptr(w_gate),
+                                      _ptr(w_up), _ptr(w_down), _ptr(dx_perm), _ptr(dw_gate),
+                                      _ptr(dw_up), _ptr(dw_down), flags, _ptr(ws), ws.numel(),
+                                      _stream()),
+           "moe_grouped_swiglu_bwd")
+    return (dx_perm if flags & MOE_BWD_DGRAD else None,
+            dw_gate if flags & MOE_BWD_WGRAD else None,
+            dw_up if flags & MOE_BWD_WGRAD else None,
+            dw_down if flags & MOE_BWD_WGRAD else None)
+
+
+# ----------------------------------------------------------------- combine
+def moe_combine(y_perm, dst, topk_gate, out=None):
+    """out[t] = sum_i gate[t,i] * y_perm[dst[t,i]] (gate None -> weight 1)."""
+    _need(y_perm, torch.bfloat16, "y_perm", 2)
+    _need(dst, torch.int32, "dst", 2)
+    if topk_gate is not None:
+        _need(topk_gate, torch.float32, "topk_gate", 2)
+    T, k = dst.shape
+    d = y_perm.shape[1]
+    if out is None:
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=y_perm.device)
+    _check(lib.moe_combine(_ptr(y_perm), _ptr(dst), _ptr(topk_gate), T, d, k, _ptr(out),
+                           _stream()), "moe_combine")
+    return out
+
+
+def moe_combine_bwd(dout, y_perm, dst, topk_gate, dy_perm=None, dgate=None, with_dgate=True):
+    """Returns (dy_perm [cap,d], dgate [T,k] or None)."""
+    _need(dout, torch.bfloat16, "dout", 2)
+    _need(y_perm, torch.bfloat16, "y_perm", 2)
+    _need(dst, torch.int32, "dst", 2)
+    if topk_gate is not None:
+        _need(topk_gate, torch.float32, "topk_gate", 2)
+    T, k = dst.shape
+    d = dout.shape[1]
+    if dy_perm is None:
+        dy_perm = torch.empty_like(y_perm)
+    if dgate is None and with_dgate:
+        dgate = torch.empty((T, k), dtype=torch.float32, device=dout.device)
+    _check(lib.moe_combine_bwd(_ptr(dout), _ptr(y_perm), _ptr(dst), _ptr(topk_gate), T, d, k,
+                               _ptr(dy_perm), _ptr(dgate), _stream()), "moe_combine_bwd")
+    return dy_perm, dgate
+
+
+# ------------------------------------------------------------- profiling
+def profile_enable(on: bool):
+    _check(lib.moe_profile_enable(1 if on else 0), "moe_profile_enable")
+
+
+def profile_reset():
+    _check(lib.moe_profile_reset(), "moe_profile_reset")
+
+
+def profile_query() -> dict:
+    """{kernel name: (total ms, launches)} over the recorded events."""
+    out = {}
+    for i in range(lib.moe_profile_num_kernels()):
+        ms = ctypes.c_double()
+        n = ctypes.c_int64()
+        _check(lib.moe_profile_query(i, ctypes.byref(ms), ctypes.byref(n)), "moe_profile_query")
+        if n.value:
+            out[lib.moe_profile_kernel_name(i).decode()] = (ms.value, n.value)
+    return out
+
+
+# ------------------------------------------------------------- whole layer
+def layer_fwd_bwd(inp: dict, k: int, expert_begin=0, num_local=None, renorm=0,
+                  keep: bool = True) -> dict:
+    """One forward + backward pass of the MoE expert layer through the C ABI.
+
+    inp: x, w_router, router_bias, w_gate, w_up, w_down, dy (device tensors).
+    Returns every intermediate (routing, permutation, activations, grads).
+    """
+    x = inp["x"]
+    E = inp["w_router"].shape[1]
+    num_local = E if num_local is None else num_local
+    idx, gate = moe_route(x, inp["w_router"], inp.get("router_bias"), k, renorm)
+    pm = moe_permute(x, idx, E, expert_begin, num_local)
+    off = pm["expert_offsets"]
+    hg, hu, y_perm = moe_grouped_swiglu_fwd(pm["x_perm"], off, inp["w_gate"], inp["w_up"],
+                                            inp["w_down"])
+    y = moe_combine(y_perm, pm["dst"], gate)
+    dy_perm, dgate = moe_combine_bwd(inp["dy"], y_perm, pm["dst"], gate)
+    dx_perm, dwg, dwu, dwd = moe_grouped_swiglu_bwd(dy_perm, pm["x_perm"], hg, hu, off,
+                                                    inp["w_gate"], inp["w_up"], inp["w_down"])
+    dx = moe_combine(dx_perm, pm["dst"], None)
+    out = {"topk_idx": idx, "topk_gate": gate, "y": y, "dgate": dgate, "dx": dx,
+           "dw_gate": dwg, "dw_up": dwu, "dw_down": dwd}
+    if keep:
+        out.update(pm)
+        out.update(h_gate=hg, h_up=hu, y_perm=y_perm, dy_perm=dy_perm, dx_perm=dx_perm)
+    return out

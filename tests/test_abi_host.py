@@ -1,0 +1,114 @@
+"""Host-side checks of the C ABI (no GPU work): the library loads, exports
+every function the header declares, answers workspace queries, and rejects
+invalid arguments on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_\w+)\s*\(", txt)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2607_01844_amd import moe
+    return moe.lib
+
+
+def _no_gpu():
+    import torch
+    return not torch.cuda.is_available()
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for want in ("moe_route", "moe_permute", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
+                 "moe_combine", "moe_combine_bwd"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    from paper_2607_01844_amd import moe
+    assert set(_declared()) == set(moe.C_SYMBOLS)
+    assert lib.moe_abi_version() == 1
+
+
+def test_status_strings(lib):
+    assert lib.moe_status_string(0) == b"MOE_OK"
+    assert lib.moe_status_string(-1) == b"MOE_ERR_INVALID_ARG"
+    assert lib.moe_status_string(-3) == b"MOE_ERR_WORKSPACE"
+
+
+def test_workspace_queries(lib):
+    n = ctypes.c_size_t()
+    assert lib.moe_route_workspace_bytes(4096, 64, ctypes.byref(n)) == 0
+    assert n.value >= 4096 * 64 * 4
+    assert lib.moe_permute_workspace_bytes(4096, 64, 6, 64, ctypes.byref(n)) == 0
+    assert n.value > 0
+    assert lib.moe_grouped_swiglu_workspace_bytes(24576, 64, 2048, 1408, 0, ctypes.byref(n)) == 0
+    fwd = n.value
+    assert fwd >= 24576 * 1408 * 2
+    assert lib.moe_grouped_swiglu_workspace_bytes(24576, 64, 2048, 1408, 3, ctypes.byref(n)) == 0
+    assert n.value >= 3 * 24576 * 1408 * 2
+    # linear in the routed rows (eq. (peaks): N k H + N_r I), never E * capacity
+    assert lib.moe_grouped_swiglu_workspace_bytes(2 * 24576, 64, 2048, 1408, 0,
+                                                  ctypes.byref(n)) == 0
+    assert n.value - fwd >= 24576 * 1408 * 2 and n.value < 2 * fwd + 4096
+    assert lib.moe_route_workspace_bytes(-1, 64, ctypes.byref(n)) == -1
+    assert lib.moe_grouped_swiglu_workspace_bytes(10, 4, 12, 16, 0, ctypes.byref(n)) == -1
+
+
+# Each case breaks exactly one rule; validation must reject it before any
+# HIP call.  Pointers are 16-byte aligned dummies that are never touched.
+P = ctypes.c_void_p(4096)
+MIS = ctypes.c_void_p(4096 + 2)
+Z = None
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="dummy pointers are only safe without a GPU")
+@pytest.mark.parametrize("case", [
+    ("k > E", lambda L: L.moe_route(P, P, Z, 10, 64, 4, 5, 0, P, P, P, Z, 0, Z)),
+    ("k > MAX_K", lambda L: L.moe_route(P, P, Z, 10, 64, 64, 17, 0, P, P, P, Z, 0, Z)),
+    ("E > MAX_E", lambda L: L.moe_route(P, P, Z, 10, 64, 2000, 2, 0, P, P, P, Z, 0, Z)),
+    ("d % 8", lambda L: L.moe_route(P, P, Z, 10, 60, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("renorm", lambda L: L.moe_route(P, P, Z, 10, 64, 8, 2, 2, P, P, P, Z, 0, Z)),
+    ("null x", lambda L: L.moe_route(Z, P, Z, 10, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("misaligned", lambda L: L.moe_route(MIS, P, Z, 10, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("T<0", lambda L: L.moe_route(P, P, Z, -1, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("T*k overflow", lambda L: L.moe_route(P, P, Z, 1 << 30, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("expert range", lambda L: L.moe_permute(P, P, 10, 64, 8, 2, 6, 3, P, Z, P, P, P, P, 1 << 20,
+                                             Z)),
+    ("num_local 0", lambda L: L.moe_permute(P, P, 10, 64, 8, 2, 0, 0, P, Z, P, P, P, P, 1 << 20,
+                                            Z)),
+    ("f % 8", lambda L: L.moe_grouped_swiglu_fwd(P, P, 4, 100, 64, 36, P, P, P, P, P, P, P,
+                                                 1 << 20, Z)),
+    ("bwd flags 0", lambda L: L.moe_grouped_swiglu_bwd(P, P, P, P, P, 4, 100, 64, 32, P, P, P, P,
+                                                       P, P, P, 0, P, 1 << 20, Z)),
+    ("bwd flags bad", lambda L: L.moe_grouped_swiglu_bwd(P, P, P, P, P, 4, 100, 64, 32, P, P, P,
+                                                         P, P, P, P, 4, P, 1 << 20, Z)),
+    ("wgrad null dw", lambda L: L.moe_grouped_swiglu_bwd(P, P, P, P, P, 4, 100, 64, 32, P, P, P,
+                                                         P, Z, P, P, 2, P, 1 << 20, Z)),
+    ("combine k", lambda L: L.moe_combine(P, P, P, 10, 64, 0, P, Z)),
+    ("combine_bwd d", lambda L: L.moe_combine_bwd(P, P, P, P, 10, 4, 2, P, P, Z)),
+])
+def test_invalid_arguments_rejected_on_host(lib, case):
+    name, call = case
+    assert call(lib) == -1, name
+    assert len(lib.moe_last_error()) > 0
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="dummy pointers are only safe without a GPU")
+def test_workspace_too_small_rejected(lib):
+    assert lib.moe_permute(P, P, 10, 64, 8, 2, 0, 8, P, Z, P, P, P, P, 16, Z) == -3
+    assert lib.moe_grouped_swiglu_fwd(P, P, 4, 100, 64, 32, P, P, P, P, P, P, P, 16, Z) == -3
+    assert lib.moe_route(P, P, Z, 10, 64, 8, 2, 0, P, P, Z, P, 16, Z) == -3

@@ -1,0 +1,182 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Small workloads are compared element by element on every tensor of one
+forward+backward pass; the full-size workloads run in the launch
+configuration the benchmark times and are compared on the complete routing
+and permutation plus sampled rows, tokens and weight-gradient entries.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _moe():
+    from paper_2607_01844_amd import moe
+    return moe
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_layer(inp, wl, poison=True):
+    """One fwd+bwd through the C ABI; outputs pre-filled with NaN / -7 so an
+    element the kernels fail to write cannot pass."""
+    moe = _moe()
+    dev = inp["x"].device
+    T, k, d, f, E, E_loc = wl.T, wl.k, wl.d, wl.f, wl.E, wl.E_loc
+    cap = wl.cap
+    nan = float("nan")
+    bf = torch.bfloat16
+
+    def full(shape, v, dt=bf):
+        return torch.full(shape, v, dtype=dt, device=dev)
+
+    idx = full((T, k), -7, torch.int32)
+    gate = full((T, k), nan, torch.float32)
+    moe.moe_route(inp["x"], inp["w_router"], inp.get("router_bias"), k, wl.renorm,
+                  topk_idx=idx, topk_gate=gate)
+    pm = moe.moe_permute(inp["x"], idx, E, wl.expert_begin, E_loc)
+    off = pm["expert_offsets"]
+    c1 = max(cap, 1)
+    hg, hu, yp = full((c1, f), nan), full((c1, f), nan), full((c1, d), nan)
+    moe.moe_grouped_swiglu_fwd(pm["x_perm"], off, inp["w_gate"], inp["w_up"], inp["w_down"],
+                               cap=cap, h_gate=hg, h_up=hu, y_perm=yp)
+    y = moe.moe_combine(yp, pm["dst"], gate, out=full((T, d), nan))
+    dyp = full((c1, d), nan)
+    _, dgate = moe.moe_combine_bwd(inp["dy"], yp, pm["dst"], gate, dy_perm=dyp,
+                                   dgate=full((T, k), nan, torch.float32))
+    dxp = full((c1, d), nan)
+    dwg = full(tuple(inp["w_gate"].shape), nan)
+    dwu = full(tuple(inp["w_up"].shape), nan)
+    dwd = full(tuple(inp["w_down"].shape), nan)
+    moe.moe_grouped_swiglu_bwd(dyp, pm["x_perm"], hg, hu, off, inp["w_gate"], inp["w_up"],
+                               inp["w_down"], cap=cap, dx_perm=dxp, dw_gate=dwg, dw_up=dwu,
+                               dw_down=dwd)
+    dx = moe.moe_combine(dxp, pm["dst"], None, out=full((T, d), nan))
+    torch.cuda.synchronize()
+    out = dict(pm)
+    out.update(topk_idx=idx, topk_gate=gate, h_gate=hg, h_up=hu, y_perm=yp, y=y, dy_perm=dyp,
+               dgate=dgate, dx_perm=dxp, dw_gate=dwg, dw_up=dwu, dw_down=dwd, dx=dx)
+    return out
+
+
+def make(wl, seed=0, bias=None, dup_cols=None):
+    inp = W.make_inputs(wl, seed=seed, device="cuda")
+    if bias is not None:
+        inp["router_bias"] = torch.tensor(bias, dtype=torch.float32, device="cuda")
+    if dup_cols is not None:  # exact logit ties: copy router columns
+        for src, dst in dup_cols:
+            inp["w_router"][:, dst] = inp["w_router"][:, src]
+    return inp
+
+
+# ------------------------------------------------------------ small, full
+SMALL = {
+    "tiny": W.WORKLOADS["tiny"],
+    "ragged": W.Workload("ragged", T=300, d=136, E=6, k=3, f=200),
+    "multi_tile": W.Workload("multi_tile", T=1100, d=520, E=4, k=2, f=328),
+    "dense_e1k1": W.Workload("dense_e1k1", T=333, d=64, E=1, k=1, f=96),
+    "k_equals_E": W.Workload("k_equals_E", T=130, d=32, E=4, k=4, f=48),
+    "ep_subset": W.Workload("ep_subset", T=400, d=64, E=16, k=2, f=64, expert_begin=5,
+                            num_local=3),
+    "renorm": W.Workload("renorm", T=256, d=128, E=8, k=3, f=64, renorm=1),
+    "t1": W.Workload("t1", T=1, d=24, E=5, k=2, f=16),
+    "min_dims": W.Workload("min_dims", T=70, d=8, E=3, k=2, f=8),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_full_parity(name):
+    wl = SMALL[name]
+    _say(f"[parity] {name} {wl.describe()}")
+    inp = make(wl)
+    gpu = run_layer(inp, wl)
+    errs = P.check_full(inp, wl, gpu)
+    _say(f"[parity] {name} ok {errs}")
+
+
+def test_skew_empty_and_full_experts():
+    """Forced-empty experts (bias -1e4) and one expert taking every token."""
+    wl = W.Workload("skew", T=700, d=96, E=8, k=2, f=80)
+    bias = np.zeros(8, np.float32)
+    bias[[2, 6]] = -1.0e4
+    bias[3] = 50.0
+    inp = make(wl, bias=bias)
+    gpu = run_layer(inp, wl)
+    errs = P.check_full(inp, wl, gpu)
+    cnt = np.diff(gpu["expert_offsets"].cpu().numpy())
+    assert cnt[2] == 0 and cnt[6] == 0 and cnt[3] == wl.T
+    _say(f"[parity] skew ok {errs}")
+
+
+def test_exact_ties_lowest_index():
+    wl = W.Workload("ties", T=200, d=64, E=8, k=3, f=32)
+    inp = make(wl, dup_cols=[(1, 4), (1, 6), (0, 7)])
+    gpu = run_layer(inp, wl)
+    P.check_full(inp, wl, gpu)
+    idx = gpu["topk_idx"].cpu().numpy()
+    # a duplicated column never precedes its lower-index twin
+    for t in range(wl.T):
+        row = list(idx[t])
+        if 4 in row and 1 in row:
+            assert row.index(1) < row.index(4)
+
+
+def test_zero_tokens():
+    moe = _moe()
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    w = torch.randn((64, 8), device="cuda")
+    idx, gate = moe.moe_route(x, w, None, 2)
+    pm = moe.moe_permute(x, idx, 8)
+    torch.cuda.synchronize()
+    assert pm["expert_offsets"].cpu().tolist() == [0] * 9
+    assert pm["counts_global"].cpu().tolist() == [0] * 8
+    wg = torch.randn((8, 64, 32), device="cuda").to(torch.bfloat16)
+    wd = torch.randn((8, 32, 64), device="cuda").to(torch.bfloat16)
+    dwg = torch.full_like(wg, float("nan"))
+    dwu = torch.full_like(wg, float("nan"))
+    dwd = torch.full_like(wd, float("nan"))
+    xp = torch.empty((1, 64), dtype=torch.bfloat16, device="cuda")
+    h = torch.empty((1, 32), dtype=torch.bfloat16, device="cuda")
+    moe.moe_grouped_swiglu_bwd(xp, xp, h, h, pm["expert_offsets"], wg, wg, wd, cap=0,
+                               dw_gate=dwg, dw_up=dwu, dw_down=dwd)
+    torch.cuda.synchronize()
+    assert torch.all(dwg == 0) and torch.all(dwu == 0) and torch.all(dwd == 0)
+
+
+def test_deterministic_bitwise():
+    wl = SMALL["multi_tile"]
+    inp = make(wl, seed=3)
+    a = run_layer(inp, wl)
+    b = run_layer(inp, wl)
+    for key in ("topk_idx", "topk_gate", "row_src", "dst", "x_perm", "y", "dgate", "dx",
+                "dw_gate", "dw_up", "dw_down"):
+        ta, tb = a[key], b[key]
+        if ta.dtype.is_floating_point:
+            ta, tb = ta.view(torch.int16 if ta.dtype == torch.bfloat16 else torch.int32), \
+                tb.view(torch.int16 if tb.dtype == torch.bfloat16 else torch.int32)
+        assert torch.equal(ta, tb), key
+
+
+# -------------------------------------------------------- full-size, sampled
+@pytest.mark.parametrize("name,full_routing", [("mid", True), ("large_skew", True),
+                                               ("ep_share", False), ("long", False)])
+def test_full_size_sampled(name, full_routing):
+    wl = W.WORKLOADS[name]
+    _say(f"[parity] {name} full size {wl.describe()}")
+    inp = make(wl)
+    gpu = run_layer(inp, wl, poison=True)
+    _say(f"[parity] {name} gpu done")
+    rng = np.random.default_rng(0)
+    errs = P.check_sampled(inp, wl, gpu, rng, full_routing=full_routing)
+    cnt = np.diff(gpu["expert_offsets"].cpu().numpy())
+    _say(f"[parity] {name} ok M={errs['M']} load={W.load_stats(cnt)} {errs}")
