@@ -152,6 +152,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (a kernel of known "
+                         "traffic, for scaling hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -207,6 +210,14 @@ def main():
                 "traffic": None, "avg_us": round(avg_s * 1e6, 2),
                 "work_per_launch": f"{flops[dom]:.4g} FLOP"}
         log(f"[bench] grouped GEMMs {gemm_tflops:.0f} TFLOP/s; dominant {dom} {ach:.0f} TFLOP/s")
+
+    if args.copy_calib_mib > 0:
+        n = args.copy_calib_mib << 20
+        src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if args.cpu_budget > 0:

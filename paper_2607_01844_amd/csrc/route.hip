@@ -4,79 +4,84 @@
 // hidden index ascending from +0.0f, then one add of the bias) so that the
 // expert choice is reproducible bit for bit.  That forbids a split of the
 // hidden dimension and any matrix-core reduction, so the logits are a
-// register-blocked SIMT fp32 kernel: each thread owns a TM x TN block of
-// (token, expert) chains; x and W_r chunks are staged through LDS.
+// register-blocked SIMT fp32 kernel: each lane owns TM x TE (token, expert)
+// chains; x and W_r chunks are staged through LDS.
 #include "common.h"
 
 namespace moe {
 namespace {
 
-constexpr int KC = 16;  // hidden-index chunk staged per LDS round
+constexpr int KC = 32;  // hidden-index chunk staged per LDS round
 
-template <int TM, int TN, int TX, int TY>
+// Lane = expert (experts lane + 64 i, i < TE), TM tokens per wave, 4 waves
+// per block (BT = 4 TM tokens).  Per hidden index j a lane reads its TE
+// router weights (LDS, distinct per lane) and the wave's TM token values
+// (LDS broadcast, fp32), then advances TM x TE independent fma chains.
+template <int TM, int TE>
 __global__ __launch_bounds__(256) void route_logits_kernel(const uint16_t* __restrict__ x,
                                                            const float* __restrict__ w,
                                                            const float* __restrict__ bias,
                                                            int64_t T, int d, int E,
                                                            float* __restrict__ logits) {
-  static_assert(TX * TY == 256, "256 threads");
-  constexpr int BT = TM * TY;  // tokens per block
-  constexpr int BE = TN * TX;  // experts per block
+  constexpr int BT = 4 * TM;
   __shared__ __align__(16) float xs[KC][BT];
-  __shared__ __align__(16) float ws[KC][BE];
-
-  const int tid = threadIdx.x;
-  const int tx = tid % TX, ty = tid / TX;
+  __shared__ __align__(16) float ws[KC][64 * TE];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t t0 = static_cast<int64_t>(blockIdx.x) * BT;
-  const int e0 = blockIdx.y * BE;
-
-  float acc[TM][TN];
+  float acc[TM][TE];
 #pragma unroll
   for (int a = 0; a < TM; ++a)
 #pragma unroll
-    for (int b = 0; b < TN; ++b) acc[a][b] = +0.0f;
+    for (int b = 0; b < TE; ++b) acc[a][b] = +0.0f;
 
   for (int j0 = 0; j0 < d; j0 += KC) {
-    const int kc = min(KC, d - j0);
-    // x chunk: BT tokens x KC hidden values, 4 bf16 (8 bytes) per load
-    for (int q = tid; q < BT * KC / 4; q += 256) {
-      const int tt = q / (KC / 4);
-      const int jq = (q % (KC / 4)) * 4;
+    const int kc = min(KC, d - j0);  // a multiple of 8
+    // x chunk -> fp32, transposed to [j][token]: 8 bf16 (16 bytes) per load
+    for (int q = tid; q < BT * (KC / 8); q += 256) {
+      const int tt = q / (KC / 8), jq = (q % (KC / 8)) * 8;
       const int64_t t = t0 + tt;
-      uint2 v = make_uint2(0u, 0u);
-      if (t < T && jq < kc) v = *reinterpret_cast<const uint2*>(x + t * d + j0 + jq);
-      xs[jq + 0][tt] = bf16_lo(v.x);
-      xs[jq + 1][tt] = bf16_hi(v.x);
-      xs[jq + 2][tt] = bf16_lo(v.y);
-      xs[jq + 3][tt] = bf16_hi(v.y);
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (t < T && jq < kc) v = *reinterpret_cast<const uint4*>(x + t * d + j0 + jq);
+      xs[jq + 0][tt] = bf16_lo(v.x); xs[jq + 1][tt] = bf16_hi(v.x);
+      xs[jq + 2][tt] = bf16_lo(v.y); xs[jq + 3][tt] = bf16_hi(v.y);
+      xs[jq + 4][tt] = bf16_lo(v.z); xs[jq + 5][tt] = bf16_hi(v.z);
+      xs[jq + 6][tt] = bf16_lo(v.w); xs[jq + 7][tt] = bf16_hi(v.w);
     }
-    // W_r chunk: KC rows x BE experts
-    for (int q = tid; q < KC * BE; q += 256) {
-      const int jj = q / BE, ee = q % BE;
-      const int e = e0 + ee;
-      ws[jj][ee] = (jj < kc && e < E) ? w[static_cast<int64_t>(j0 + jj) * E + e] : 0.0f;
+    // W_r chunk: KC rows x (64 TE) experts, coalesced along experts
+    for (int q = tid; q < KC * 64 * TE; q += 256) {
+      const int jj = q / (64 * TE), ee = q % (64 * TE);
+      ws[jj][ee] = (jj < kc && ee < E) ? w[static_cast<int64_t>(j0 + jj) * E + ee] : 0.0f;
     }
     __syncthreads();
-    for (int jj = 0; jj < kc; ++jj) {
-      float xv[TM], wv[TN];
+    auto step = [&](int jj) {
+      float xv[TM], wr[TE];
 #pragma unroll
-      for (int a = 0; a < TM; ++a) xv[a] = xs[jj][ty * TM + a];
+      for (int a = 0; a < TM; ++a) xv[a] = xs[jj][wv * TM + a];  // broadcast
 #pragma unroll
-      for (int b = 0; b < TN; ++b) wv[b] = ws[jj][tx * TN + b];
+      for (int b = 0; b < TE; ++b) wr[b] = ws[jj][lane + 64 * b];
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < TN; ++b) acc[a][b] = __builtin_fmaf(xv[a], wv[b], acc[a][b]);
+        for (int b = 0; b < TE; ++b) acc[a][b] = __builtin_fmaf(xv[a], wr[b], acc[a][b]);
+    };
+    if (kc == KC) {
+#pragma unroll
+      for (int jj = 0; jj < KC; ++jj) step(jj);
+    } else {
+      for (int j8 = 0; j8 < kc; j8 += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) step(j8 + u);
+      }
     }
     __syncthreads();
   }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
-    const int64_t t = t0 + ty * TM + a;
+    const int64_t t = t0 + wv * TM + a;
     if (t >= T) continue;
 #pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      const int e = e0 + tx * TN + b;
+    for (int b = 0; b < TE; ++b) {
+      const int e = lane + 64 * b;
       if (e >= E) continue;
       float v = acc[a][b];
       if (bias) v = v + bias[e];
@@ -154,15 +159,24 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   }
 }
 
-template <int TM, int TN, int TX, int TY>
+template <int TM, int TE>
 hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                       int E, float* logits, hipStream_t s) {
-  constexpr int BT = TM * TY, BE = TN * TX;
-  dim3 grid(static_cast<unsigned>(ceil_div(T, BT)), static_cast<unsigned>(ceil_div(E, BE)));
+  const unsigned grid = static_cast<unsigned>(ceil_div(T, 4 * TM));
   prof_begin(K_ROUTE_LOGITS, s);
-  route_logits_kernel<TM, TN, TX, TY><<<grid, 256, 0, s>>>(x, w, bias, T, d, E, logits);
+  route_logits_kernel<TM, TE><<<grid, 256, 0, s>>>(x, w, bias, T, d, E, logits);
   prof_end(K_ROUTE_LOGITS, s);
   return hipGetLastError();
+}
+
+// Tokens per wave: the largest of 8, 4, 2 that still gives every CU a
+// workgroup.
+template <int TE>
+hipError_t pick_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
+                       int E, float* logits, hipStream_t s) {
+  if (ceil_div(T, 32) >= 256) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
+  if (ceil_div(T, 16) >= 256) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
+  return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
 }
 
 }  // namespace
@@ -171,16 +185,12 @@ hipError_t launch_route(const uint16_t* x, const float* w, const float* bias, in
                         int E, int k, int renorm, int32_t* idx, float* gate, float* logits,
                         hipStream_t s) {
   if (T == 0) return hipSuccess;
-  // Largest register block that still gives >= 2 blocks per CU.
-  const int64_t want = 512;
   hipError_t err;
-  auto nblk = [&](int bt, int be) { return ceil_div(T, bt) * ceil_div(E, be); };
-  if (nblk(64, 128) >= want && E > 64)
-    err = run_logits<8, 4, 32, 8>(x, w, bias, T, d, E, logits, s);
-  else if (nblk(64, 64) >= want)
-    err = run_logits<4, 4, 16, 16>(x, w, bias, T, d, E, logits, s);
-  else
-    err = run_logits<2, 2, 16, 16>(x, w, bias, T, d, E, logits, s);
+  if (E <= 64) err = pick_logits<1>(x, w, bias, T, d, E, logits, s);
+  else if (E <= 128) err = pick_logits<2>(x, w, bias, T, d, E, logits, s);
+  else if (E <= 256) err = pick_logits<4>(x, w, bias, T, d, E, logits, s);
+  else if (E <= 512) err = pick_logits<8>(x, w, bias, T, d, E, logits, s);
+  else err = pick_logits<16>(x, w, bias, T, d, E, logits, s);
   if (err != hipSuccess) return err;
 
   const unsigned grid = static_cast<unsigned>(ceil_div(T, 4));
