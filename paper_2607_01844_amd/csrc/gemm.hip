@@ -10,14 +10,16 @@
 //     register staging).  The buffer descriptor's range check turns every
 //     tail (rows past an expert's segment, k past K, columns past N) into
 //     zeros, so there is no padding and no per-element branching.
-//   * K steps of 32 in a ring of 4 LDS stages (128 KiB of the 160 KiB):
-//     loads run three steps ahead of the MFMAs; one barrier per step.
+//   * K steps of 64 in a ring of 2 LDS stages (128 KiB of the 160 KiB):
+//     loads run one step ahead of the MFMAs; one barrier per step.  A step
+//     of 64 k makes every row of a K-contiguous tile one full 128-byte line,
+//     which the memory path moves at twice the rate of 64-byte halves.
 //   * Operands stored K-contiguous (activations in the forward pass and the
 //     data gradients, weights in the data gradients) sit in LDS as
-//     [256 rows][32 k] and feed the MFMA with ds_read_b128.  Operands stored
+//     [256 rows][64 k] and feed the MFMA with ds_read_b128.  Operands stored
 //     with the output index contiguous (weights in the forward pass,
 //     everything in the weight gradients) keep that layout in LDS
-//     ([32 k][128 cols] sub-tiles) and are read with ds_read_b64_tr_b16,
+//     ([64 k][128 cols] sub-tiles) and are read with ds_read_b64_tr_b16,
 //     which transposes 4 x 16 blocks across each group of 16 lanes.
 //     Both layouts carry a 16-byte-chunk XOR swizzle that makes the
 //     fragment reads conflict-free.
@@ -37,11 +39,13 @@ namespace {
 
 constexpr int BM = 256;      // tile rows on the operand-A side (m)
 constexpr int BN = 256;      // tile rows on the operand-B side (n)
-constexpr int BK = 32;       // k per pipeline stage
-constexpr int NST = 4;       // LDS stages
-constexpr int OP_BYTES = 256 * BK * 2;     // one operand tile per stage (16 KiB)
-constexpr int STAGE_BYTES = 2 * OP_BYTES;  // A + B (32 KiB)
-constexpr int LOADS = 4;     // 16-byte direct loads per lane, per operand and stage
+constexpr int BK = 64;       // k per step (128-byte rows of a K-contiguous tile)
+constexpr int UNIT = 256 * BK * 2;  // one operand tile of one step in LDS (32 KiB)
+constexpr int HALF = UNIT / 2;      // half a step (32 k) of an N-contiguous tile
+constexpr int LOADS_K = 8;   // 16-byte direct loads per lane: K-contiguous unit
+constexpr int LOADS_H = 4;   //                                N-contiguous half
+constexpr int NRING = 5;     // LDS ring slots of UNIT bytes (160 KiB)
+constexpr int PATCH_BYTES = 8192;  // per-wave epilogue staging
 constexpr int NXCD = 8;
 constexpr uint32_t OOB = 0x80000000u;  // buffer offset past every range: reads as zero
 
@@ -87,17 +91,57 @@ __device__ __forceinline__ void load_lds16(const i32x4& rsrc, uint32_t voff, uin
 }
 #pragma clang diagnostic pop
 
+// A value the optimiser cannot see through: per-lane load offsets derived
+// from it are recomputed at each issue instead of being hoisted out of the
+// K loop, where they would be spilled and reloaded (and a scratch reload
+// waits for every load in flight).
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// Compiler-visible s_waitcnt lgkmcnt(0) (vmcnt and expcnt left at their
+// maximum): after code that may have issued scalar loads (kernel arguments,
+// schedule tables), so that the waitcnt pass, which must assume such loads
+// return out of order, does not turn the next fragment wait into a full one.
+__device__ __forceinline__ void lgkm_drained() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
 }
 
+typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));
+// Eight 16-byte loads into registers (four from each of two buffers) that
+// complete inside the statement: the compiler never sees them in flight, so
+// its own counter bookkeeping stays exact around the K loop.  Waits for
+// every vector-memory operation of the wave.
+__device__ __forceinline__ void load_2x4_wait(const i32x4& ra, const i32x4& rb, const uint32_t (&off)[4],
+                                              u32x4a (&a)[4], u32x4a (&b)[4]) {
+  asm volatile(
+      "buffer_load_dwordx4 %0, %8, %12, 0 offen\n\t"
+      "buffer_load_dwordx4 %1, %9, %12, 0 offen\n\t"
+      "buffer_load_dwordx4 %2, %10, %12, 0 offen\n\t"
+      "buffer_load_dwordx4 %3, %11, %12, 0 offen\n\t"
+      "buffer_load_dwordx4 %4, %8, %13, 0 offen\n\t"
+      "buffer_load_dwordx4 %5, %9, %13, 0 offen\n\t"
+      "buffer_load_dwordx4 %6, %10, %13, 0 offen\n\t"
+      "buffer_load_dwordx4 %7, %11, %13, 0 offen\n\t"
+      "s_waitcnt vmcnt(0)"
+      : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3]), "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]),
+        "=&v"(b[3])
+      : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(ra), "s"(rb)
+      : "memory");
+}
+
 // ------------------------------------------------------- K-major operand
 // Tile rows r (m or n) with k contiguous: element (r, k) of source s at
 // byte r*ld + 2k from its base.  Dual-K: steps [0, nk0) read source 0,
-// steps [nk0, nk) source 1 (k restarts at 0).  LDS: [256][32] bf16,
-// 64-byte rows, chunk c of row r at ((c ^ ((r >> 1) & 3)) << 4).
-__device__ __forceinline__ int koff(int r, int c) { return r * (BK * 2) + ((c ^ ((r >> 1) & 3)) << 4); }
+// steps [nk0, nk) source 1 (k restarts at 0).  LDS: [256][64] bf16,
+// 128-byte rows, 16-byte chunk c of row r at ((c ^ ((r / 2) % 8)) << 4): the
+// 16 rows one ds_read_b128 pass covers (64 banks of 4 bytes) hit 16
+// different 16-byte bank groups.
+__device__ __forceinline__ int koff(int r, int c) { return r * (BK * 2) + ((c ^ ((r >> 1) & 7)) << 4); }
 
 struct KOperand {
   i32x4 rsrc0, rsrc1;
@@ -106,21 +150,53 @@ struct KOperand {
   int kmax0, kmax1; // valid k of source 0 / 1
   int nk0;          // steps of source 0
 
-  // Per load q (0..3) of this wave, lane l covers tile row
-  // r = 16 (4 wave + q) + l / 4 and 16-byte chunk lc = (l % 4) ^ ((r / 2) % 4).
-  __device__ __forceinline__ void issue(int kt, uint32_t lds_op, int wave, int lane) const {
+  // Load q (0..7) of this wave, I = 8 wave + q, fills tile rows 8 I .. 8 I + 7:
+  // lane l takes row r = 8 I + l / 8 and 16-byte chunk lc = (l % 8) ^ ((r / 2) % 8),
+  // where (r / 2) % 8 = 4 (q % 2) + l / 16.  prep() computes what the eight
+  // loads of one step share; Issue::emit(q) sends load q, so that the loads
+  // can be spread between MFMAs.
+  struct Issue {
+    i32x4 rs;
+    uint32_t ld, lds;     // row pitch; LDS base of the unit
+    uint32_t vb0, vb1;    // lane offsets of even / odd loads
+    int rows, rl;         // valid tile rows; this lane's row within a load
+    bool kok0, kok1;      // this lane's chunk lies below K (even / odd loads)
+    __device__ __forceinline__ void emit(int q, int wave) const {
+      const int r0 = (wave * LOADS_K + q) * 8;
+      const bool ok = ((q & 1) ? kok1 : kok0) && rl < rows - r0;
+      load_lds16(rs, ok ? ((q & 1) ? vb1 : vb0) + static_cast<uint32_t>(r0) * ld : OOB,
+                 lds + (wave * LOADS_K + q) * 1024);
+    }
+  };
+  __device__ __forceinline__ Issue prep(int kt, uint32_t lds_op, int lane_in) const {
     const bool s1 = kt >= nk0;
     const int k0 = (s1 ? kt - nk0 : kt) * BK;
     const int km = s1 ? kmax1 : kmax0;
-    const i32x4 rs = s1 ? rsrc1 : rsrc0;
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q) {
-      const int r = (wave * LOADS + q) * 16 + (lane >> 2);
-      const int lc = (lane & 3) ^ ((r >> 1) & 3);
-      const bool ok = r < rows && k0 + lc * 8 < km;
-      const uint32_t v = static_cast<uint32_t>(r) * ld + static_cast<uint32_t>(lc * 16 + k0 * 2);
-      load_lds16(rs, ok ? v : OOB, lds_op + (wave * LOADS + q) * 1024);
-    }
+    Issue p;
+    p.rs = s1 ? rsrc1 : rsrc0;
+    const int lane = opaque(lane_in);
+    p.rl = lane >> 3;
+    const int lc0 = (lane & 7) ^ (lane >> 4);      // chunk fetched by even loads
+    const int lc1 = lc0 ^ 4;                       //                 odd loads
+    p.kok0 = k0 + lc0 * 8 < km;
+    p.kok1 = k0 + lc1 * 8 < km;
+    const uint32_t rb = static_cast<uint32_t>(p.rl) * ld + static_cast<uint32_t>(k0 * 2);
+    p.vb0 = rb + static_cast<uint32_t>(lc0 * 16);
+    p.vb1 = rb + static_cast<uint32_t>(lc1 * 16);
+    p.ld = ld;
+    p.rows = rows;
+    p.lds = lds_op;
+    return p;
+  }
+  // the same number of loads, all out of range (zeros into an unused slot)
+  static __device__ __forceinline__ Issue none(const i32x4& nil, uint32_t lds_op) {
+    Issue p;
+    p.rs = nil;
+    p.ld = p.vb0 = p.vb1 = 0;
+    p.rows = p.rl = 0;
+    p.kok0 = p.kok1 = false;
+    p.lds = lds_op;
+    return p;
   }
   // MFMA fragment: 8 consecutive k (k-group `kg` of substep s) of tile row r
   static __device__ __forceinline__ bf16x8 frag(const lds_char* t, int r, int s, int kg) {
@@ -132,11 +208,14 @@ struct KOperand {
 // Stored [k][cols] with the tile index contiguous: element (k, c) at byte
 // k*ld + 2c of the sub-tile's base.  The tile's 256 columns are two
 // sub-tiles of 128 (sub-tile j starts at ptr_j, has cols_j valid columns and
-// range_j readable bytes); k < kmax valid.  The descriptor base advances
-// with the K step, so lane offsets stay below 32 rows.  LDS: per sub-tile
-// [32][128] bf16, 256-byte rows, chunk c of row k at ((c ^ (2 (k & 3))) << 4).
+// range_j readable bytes); k < kmax valid.  Loads move half a step (32 k)
+// at a time, so that the half consumed first is refilled half a step
+// earlier.  The descriptor base advances with k, so lane offsets stay below
+// 32 rows.  LDS per half: two sub-tiles [32 k][128 cols] bf16, 256-byte
+// rows, 16-byte chunk c of row k at ((c ^ (4 (k & 3))) << 4): the 32 lanes of
+// one ds_read_b64_tr_b16 pass (4 rows x 4 chunks x 2 halves) hit all 64 banks.
 __device__ __forceinline__ int noff(int k, int col) {
-  return k * 256 + ((((col >> 3) ^ (2 * (k & 3)))) << 4) + ((col >> 2) & 1) * 8;
+  return k * 256 + ((((col >> 3) ^ (4 * (k & 3)))) << 4) + ((col >> 2) & 1) * 8;
 }
 
 struct NOperand {
@@ -147,34 +226,56 @@ struct NOperand {
   int cols0, cols1;
   int kmax;
 
-  // Per load q (0..3) of this wave: instruction I = 4 wave + q covers rows
-  // 4 (I % 8) .. +3 of sub-tile I / 8; lane l takes row k = 4 (I % 8) + l / 16
-  // and column 8 ((l % 16) ^ (2 (k % 4))).
-  __device__ __forceinline__ void issue(int kt, uint32_t lds_op, int wave, int lane) const {
-    const int k0 = kt * BK;
-    const int64_t adv = static_cast<int64_t>(k0) * ld;
-    const i32x4 r0 = make_rsrc(reinterpret_cast<const char*>(ptr0) + adv, range0 - adv);
-    const i32x4 r1 = make_rsrc(reinterpret_cast<const char*>(ptr1) + adv, range1 - adv);
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q) {
-      const int I = wave * LOADS + q;
-      const int k = (I & 7) * 4 + (lane >> 4);
-      const int col = ((lane & 15) ^ (2 * (k & 3))) * 8;
-      const bool ok = col < ((I >> 3) ? cols1 : cols0) && k0 + k < kmax;
-      const uint32_t v = static_cast<uint32_t>(k) * ld + static_cast<uint32_t>(col) * 2u;
-      load_lds16((I >> 3) ? r1 : r0, ok ? v : OOB,
-                 lds_op + (I >> 3) * (OP_BYTES / 2) + (I & 7) * 1024);
+  // Half h (0, 1) of step kt.  Load q (0..3) of this wave: I = 4 wave + q
+  // covers rows 4 (I % 8) .. +3 of sub-tile I / 8; lane l takes row
+  // k = 4 (I % 8) + l / 16 and column 8 ((l % 16) ^ (4 (k % 4))).
+  struct Issue {
+    i32x4 r0, r1;
+    uint32_t ld, lds, vb;
+    int col, cols0, cols1, krem, kl;
+    __device__ __forceinline__ void emit(int q, int wave) const {
+      const int I = wave * LOADS_H + q;
+      const int kr = (I & 7) * 4;
+      const bool ok = col < ((I >> 3) ? cols1 : cols0) && kl < krem - kr;
+      load_lds16((I >> 3) ? r1 : r0, ok ? vb + static_cast<uint32_t>(kr) * ld : OOB,
+                 lds + (I >> 3) * (HALF / 2) + (I & 7) * 1024);
     }
+  };
+  __device__ __forceinline__ Issue prep(int kt, int h, uint32_t lds_half, int lane_in) const {
+    const int k0 = kt * BK + h * (BK / 2);
+    const int64_t adv = static_cast<int64_t>(k0) * ld;
+    Issue p;
+    p.r0 = make_rsrc(reinterpret_cast<const char*>(ptr0) + adv, range0 - adv);
+    p.r1 = make_rsrc(reinterpret_cast<const char*>(ptr1) + adv, range1 - adv);
+    const int lane = opaque(lane_in);
+    p.kl = lane >> 4;                                // row within the load's 4 rows
+    p.col = ((lane & 15) ^ (4 * p.kl)) * 8;          // (row % 4 == kl)
+    p.vb = static_cast<uint32_t>(p.kl) * ld + static_cast<uint32_t>(p.col) * 2u;
+    p.ld = ld;
+    p.cols0 = cols0;
+    p.cols1 = cols1;
+    p.krem = kmax - k0;
+    p.lds = lds_half;
+    return p;
   }
-  // MFMA fragment of tile column block c0 (multiple of 32): lane l gets
-  // 8 consecutive k (k-group l/32 of substep s) of column c0 + l%32, built
-  // from two transposing reads of 4 k each.
+  static __device__ __forceinline__ Issue none(const i32x4& nil, uint32_t lds_half) {
+    Issue p;
+    p.r0 = p.r1 = nil;
+    p.ld = p.vb = 0;
+    p.col = p.kl = p.krem = 0;
+    p.cols0 = p.cols1 = 0;
+    p.lds = lds_half;
+    return p;
+  }
+  // MFMA fragment of tile column block c0 (multiple of 32) from one half:
+  // lane l gets 8 consecutive k (k-group l/32 of substep s, 0..1, of the
+  // half) of column c0 + l%32, built from two transposing reads of 4 k each.
   static __device__ __forceinline__ bf16x8 frag(const lds_char* t, int c0, int s, int lane) {
     const int g = lane >> 4, r = lane & 15;
     const int st = c0 >> 7;
     const int col = (c0 & 127) + 16 * (g & 1) + 4 * (r & 3);
     const int k = 16 * s + 8 * (g >> 1) + (r >> 2);
-    const lds_char* b = t + st * (OP_BYTES / 2);
+    const lds_char* b = t + st * (HALF / 2);
     const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
         (__attribute__((address_space(3))) s16x4*)(b + noff(k, col)));
     const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -240,13 +341,21 @@ struct Tile {
 //    rows, descending) are dealt to XCDs in snake order (0..7, 7..0, ...),
 //    which balances skewed loads and spreads a large expert over all XCDs;
 //    the column tiles of a group are adjacent on its XCD.
-// Schedule tables of one launch, copied to LDS at kernel start: tile
-// decoding then never waits on the vector-memory counter, which the
-// in-flight operand loads use.
+// Schedule tables of one launch, read with scalar loads: tile decoding is
+// uniform, and a scalar load waits on the LDS/scalar counter only, never on
+// the vector-memory counter that tracks the operand loads in flight.
+__device__ __forceinline__ int sld(const int32_t* p) {
+  int v;
+  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
+  return v;
+}
 struct Tables {
-  const int* mt_start;  // [E_loc + 1]
-  const int* offsets;   // [E_loc + 1]
-  const int* lpt;       // [E_loc]
+  const int32_t* mt_start_;  // [E_loc + 1]
+  const int32_t* offsets_;   // [E_loc + 1]
+  const int32_t* lpt_;       // [E_loc]
+  __device__ __forceinline__ int mt(int i) const { return sld(mt_start_ + i); }
+  __device__ __forceinline__ int off(int i) const { return sld(offsets_ + i); }
+  __device__ __forceinline__ int lpt(int i) const { return sld(lpt_ + i); }
 };
 
 template <int MODE>
@@ -265,7 +374,7 @@ struct TileIter {
     j = blockIdx.x / NXCD;
     i = 0;
     if constexpr (!WG) {
-      total = tb.mt_start[g.E_loc] * g.NT;
+      total = tb.mt(g.E_loc) * g.NT;
       const int per = (total + NXCD - 1) / NXCD;
       end = min((xcd + 1) * per, total);
       total = xcd * per;  // start of this XCD's range
@@ -284,16 +393,16 @@ struct TileIter {
       int lo = 0, hi = g.E_loc;
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (tb.mt_start[mid] * g.NT <= L) lo = mid; else hi = mid;
+        if (tb.mt(mid) * g.NT <= L) lo = mid; else hi = mid;
       }
       t.e = __builtin_amdgcn_readfirstlane(lo);
-      const int ms0 = __builtin_amdgcn_readfirstlane(tb.mt_start[lo]);
-      const int mt_e = __builtin_amdgcn_readfirstlane(tb.mt_start[lo + 1]) - ms0;
+      const int ms0 = tb.mt(lo);
+      const int mt_e = tb.mt(lo + 1) - ms0;
       const int local = L - ms0 * g.NT;
       t.m0 = (local % mt_e) * BM;
       t.n0 = (local / mt_e) * (DUAL ? BN / 2 : BN);
-      t.seg = __builtin_amdgcn_readfirstlane(tb.offsets[lo]);
-      t.ne = __builtin_amdgcn_readfirstlane(tb.offsets[lo + 1]) - t.seg;
+      t.seg = tb.off(lo);
+      t.ne = tb.off(lo + 1) - t.seg;
       const int K = (MODE == FWD_GATE_UP || MODE == DGRAD_DOWN) ? g.d : g.f;
       t.nk = ((K + BK - 1) / BK) * (MODE == DGRAD_GATE_UP ? 2 : 1);
       t.valid = true;
@@ -306,11 +415,11 @@ struct TileIter {
         const int k = lt / g.NT, nt = lt % g.NT;
         const int q = 16 * (k >> 1) + ((k & 1) ? 15 - xcd : xcd);
         if (q >= gq) continue;
-        t.e = __builtin_amdgcn_readfirstlane(tb.lpt[q / g.MT]);
+        t.e = tb.lpt(q / g.MT);
         t.m0 = (q % g.MT) * BM;
         t.n0 = nt * (DUAL ? BN / 2 : BN);
-        t.seg = __builtin_amdgcn_readfirstlane(tb.offsets[t.e]);
-        t.ne = __builtin_amdgcn_readfirstlane(tb.offsets[t.e + 1]) - t.seg;
+        t.seg = tb.off(t.e);
+        t.ne = tb.off(t.e + 1) - t.seg;
         t.nk = (t.ne + BK - 1) / BK;
         if (t.nk == 0 && !zeros) continue;
         if (t.nk != 0 && zeros) continue;
@@ -323,8 +432,7 @@ struct TileIter {
 
 template <int MODE>
 __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
-  __shared__ __align__(1024) char lds[NST * STAGE_BYTES];
-  __shared__ int tab[3 * MOE_MAX_E + 2];
+  __shared__ __align__(1024) char lds[NRING * UNIT];
   constexpr bool WGRAD = (MODE == WGRAD_GATE_UP || MODE == WGRAD_DOWN);
   constexpr bool DUAL = (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP);
   constexpr bool A_N = WGRAD;                                        // A side N-major?
@@ -341,49 +449,59 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
 
   // ------------------------------------------------------- operand setup
   // A side = rows m of the output, B side = columns n of the output.
-  auto setup = [&](const Tile& tl, AOp& A, BOp& B) __attribute__((always_inline)) {
-    const int e = tl.e, m0 = tl.m0, n0 = tl.n0, seg = tl.seg, ne = tl.ne;
+  auto setupA = [&](const Tile& tl, AOp& A) __attribute__((always_inline)) {
+    const int m0 = tl.m0, seg = tl.seg, ne = tl.ne;
     if constexpr (MODE == FWD_GATE_UP) {
       const uint16_t* xa = g.x_perm + (int64_t)(seg + m0) * d;
       A.rsrc0 = A.rsrc1 = make_rsrc(xa, (int64_t)(ne - m0) * d * 2);
       A.ld = d * 2; A.rows = ne - m0; A.kmax0 = A.kmax1 = d; A.nk0 = (d + BK - 1) / BK;
-      B.ptr0 = g.wg + e * wdf + n0; B.range0 = (wdf - n0) * 2;
-      B.ptr1 = g.wu + e * wdf + n0; B.range1 = (wdf - n0) * 2;
-      B.ld = f * 2; B.cols0 = B.cols1 = f - n0; B.kmax = d;
     } else if constexpr (MODE == FWD_DOWN) {
       const uint16_t* aa = g.act_in + (int64_t)(seg + m0) * f;
       A.rsrc0 = A.rsrc1 = make_rsrc(aa, (int64_t)(ne - m0) * f * 2);
       A.ld = f * 2; A.rows = ne - m0; A.kmax0 = A.kmax1 = f; A.nk0 = (f + BK - 1) / BK;
-      B.ptr0 = g.wd + e * wdf + n0; B.range0 = (wdf - n0) * 2;
-      B.ptr1 = B.ptr0 + 128; B.range1 = (wdf - n0 - 128) * 2;
-      B.ld = d * 2; B.cols0 = d - n0; B.cols1 = d - n0 - 128; B.kmax = f;
     } else if constexpr (MODE == DGRAD_DOWN) {
       const uint16_t* ya = g.dy + (int64_t)(seg + m0) * d;
       A.rsrc0 = A.rsrc1 = make_rsrc(ya, (int64_t)(ne - m0) * d * 2);
       A.ld = d * 2; A.rows = ne - m0; A.kmax0 = A.kmax1 = d; A.nk0 = (d + BK - 1) / BK;
-      const uint16_t* wb = g.wd + e * wdf + (int64_t)n0 * d;
-      B.rsrc0 = B.rsrc1 = make_rsrc(wb, (int64_t)(f - n0) * d * 2);
-      B.ld = d * 2; B.rows = f - n0; B.kmax0 = B.kmax1 = d; B.nk0 = A.nk0;
     } else if constexpr (MODE == DGRAD_GATE_UP) {
       const int64_t ro = (int64_t)(seg + m0) * f;
       A.rsrc0 = make_rsrc(g.dhg_in + ro, (int64_t)(ne - m0) * f * 2);
       A.rsrc1 = make_rsrc(g.dhu_in + ro, (int64_t)(ne - m0) * f * 2);
       A.ld = f * 2; A.rows = ne - m0; A.kmax0 = A.kmax1 = f; A.nk0 = (f + BK - 1) / BK;
-      const int64_t wo = e * wdf + (int64_t)n0 * f;
-      B.rsrc0 = make_rsrc(g.wg + wo, (int64_t)(d - n0) * f * 2);
-      B.rsrc1 = make_rsrc(g.wu + wo, (int64_t)(d - n0) * f * 2);
-      B.ld = f * 2; B.rows = d - n0; B.kmax0 = B.kmax1 = f; B.nk0 = A.nk0;
     } else if constexpr (MODE == WGRAD_GATE_UP) {
       A.ptr0 = g.x_perm + (int64_t)seg * d + m0; A.range0 = ((int64_t)ne * d - m0) * 2;
       A.ptr1 = A.ptr0 + 128; A.range1 = A.range0 - 256;
       A.ld = d * 2; A.cols0 = d - m0; A.cols1 = d - m0 - 128; A.kmax = ne;
-      B.ptr0 = g.dhg_in + (int64_t)seg * f + n0; B.range0 = ((int64_t)ne * f - n0) * 2;
-      B.ptr1 = g.dhu_in + (int64_t)seg * f + n0; B.range1 = B.range0;
-      B.ld = f * 2; B.cols0 = B.cols1 = f - n0; B.kmax = ne;
     } else {  // WGRAD_DOWN
       A.ptr0 = g.act_in + (int64_t)seg * f + m0; A.range0 = ((int64_t)ne * f - m0) * 2;
       A.ptr1 = A.ptr0 + 128; A.range1 = A.range0 - 256;
       A.ld = f * 2; A.cols0 = f - m0; A.cols1 = f - m0 - 128; A.kmax = ne;
+    }
+  };
+  auto setupB = [&](const Tile& tl, BOp& B) __attribute__((always_inline)) {
+    const int e = tl.e, n0 = tl.n0, seg = tl.seg, ne = tl.ne;
+    if constexpr (MODE == FWD_GATE_UP) {
+      B.ptr0 = g.wg + e * wdf + n0; B.range0 = (wdf - n0) * 2;
+      B.ptr1 = g.wu + e * wdf + n0; B.range1 = (wdf - n0) * 2;
+      B.ld = f * 2; B.cols0 = B.cols1 = f - n0; B.kmax = d;
+    } else if constexpr (MODE == FWD_DOWN) {
+      B.ptr0 = g.wd + e * wdf + n0; B.range0 = (wdf - n0) * 2;
+      B.ptr1 = B.ptr0 + 128; B.range1 = (wdf - n0 - 128) * 2;
+      B.ld = d * 2; B.cols0 = d - n0; B.cols1 = d - n0 - 128; B.kmax = f;
+    } else if constexpr (MODE == DGRAD_DOWN) {
+      const uint16_t* wb = g.wd + e * wdf + (int64_t)n0 * d;
+      B.rsrc0 = B.rsrc1 = make_rsrc(wb, (int64_t)(f - n0) * d * 2);
+      B.ld = d * 2; B.rows = f - n0; B.kmax0 = B.kmax1 = d; B.nk0 = (d + BK - 1) / BK;
+    } else if constexpr (MODE == DGRAD_GATE_UP) {
+      const int64_t wo = e * wdf + (int64_t)n0 * f;
+      B.rsrc0 = make_rsrc(g.wg + wo, (int64_t)(d - n0) * f * 2);
+      B.rsrc1 = make_rsrc(g.wu + wo, (int64_t)(d - n0) * f * 2);
+      B.ld = f * 2; B.rows = d - n0; B.kmax0 = B.kmax1 = f; B.nk0 = (f + BK - 1) / BK;
+    } else if constexpr (MODE == WGRAD_GATE_UP) {
+      B.ptr0 = g.dhg_in + (int64_t)seg * f + n0; B.range0 = ((int64_t)ne * f - n0) * 2;
+      B.ptr1 = g.dhu_in + (int64_t)seg * f + n0; B.range1 = B.range0;
+      B.ld = f * 2; B.cols0 = B.cols1 = f - n0; B.kmax = ne;
+    } else {  // WGRAD_DOWN
       B.ptr0 = g.dy + (int64_t)seg * d + n0; B.range0 = ((int64_t)ne * d - n0) * 2;
       B.ptr1 = B.ptr0 + 128; B.range1 = B.range0 - 256;
       B.ld = d * 2; B.cols0 = d - n0; B.cols1 = d - n0 - 128; B.kmax = ne;
@@ -412,100 +530,196 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
 
   // ------------------------------------------------------------ epilogue
   // acc[i][j][4q + u]: output row m = arow[i] + l32 (tile-relative),
-  // output column n = brow[j] + 8q + 4*lh + u.
-  auto epilogue = [&](const Tile& tl) __attribute__((always_inline)) {
+  // output column n = brow[j] + 8q + 4*lh + u.  Each wave passes its
+  // 128 x 128 block through its own 8 KiB LDS patch, 32 rows (16 in fp32)
+  // at a time: it writes the accumulators in the MFMA layout and reads them
+  // back row-major, so that every global access moves 16 bytes per lane
+  // and 8 or 16 lanes cover one contiguous row segment (whole 128-byte
+  // lines instead of 32 scattered 16-byte pieces per instruction).  Patch
+  // chunks carry an XOR swizzle on the row index.
+  auto epilogue = [&](const Tile& tl, lds_char* patch) __attribute__((always_inline)) {
     const int e = tl.e, m0 = tl.m0, n0 = tl.n0, seg = tl.seg, ne = tl.ne;
-    int arow[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) arow[i] = wm * 128 + 32 * i + l32;
-  const int mvalid = WGRAD ? ((MODE == WGRAD_GATE_UP ? d : f) - m0) : (ne - m0);
+    // lane-derived indices recomputed here (not hoisted and kept live
+    // across the K loop, where they would be spilled)
+    const int lane = opaque(threadIdx.x & 63);
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int mvalid = WGRAD ? ((MODE == WGRAD_GATE_UP ? d : f) - m0) : (ne - m0);
+    typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+    typedef float f32x4v __attribute__((ext_vector_type(4)));
+    auto put8 = [&](int off, uint2 v) __attribute__((always_inline)) {
+      *(__attribute__((address_space(3))) u32x2v*)(patch + off) = u32x2v{v.x, v.y};
+    };
+    auto put16 = [&](int off, float4 v) __attribute__((always_inline)) {
+      *(__attribute__((address_space(3))) f32x4v*)(patch + off) = f32x4v{v.x, v.y, v.z, v.w};
+    };
+    auto get16 = [&](int off) __attribute__((always_inline)) {
+      const u32x4v v = *(__attribute__((address_space(3))) u32x4v*)(patch + off);
+      return make_uint4(v[0], v[1], v[2], v[3]);
+    };
+    auto getf16 = [&](int off) __attribute__((always_inline)) {
+      const f32x4v v = *(__attribute__((address_space(3))) f32x4v*)(patch + off);
+      return make_float4(v[0], v[1], v[2], v[3]);
+    };
+    auto fence = []() __attribute__((always_inline)) { asm volatile("" ::: "memory"); };
+    auto unswap = [](uint4 v, int r) __attribute__((always_inline)) {
+      return (r & 16) ? make_uint4(v.z, v.w, v.x, v.y) : v;
+    };
     static_for<4>([&](auto I) {
       constexpr int i = I;
-      const int m = arow[i];
-      if (m < mvalid) {
-        if constexpr (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP) {
-          static_for<2>([&](auto J) {
-            constexpr int j = J;
-            static_for<4>([&](auto Q) {
-              constexpr int q = Q;
-              const int n = wn * 64 + 32 * j + 8 * q + 4 * lh;  // f index within tile
-              if (n0 + n < f) {
-                const f32x16& ga = acc[i][j];
-                const f32x16& ua = acc[i][j + 2];
-                if constexpr (MODE == FWD_GATE_UP) {
-                  const int64_t o = (int64_t)(seg + m0 + m) * f + n0 + n;
-                  const uint2 hgb = pack4(ga[4 * q], ga[4 * q + 1], ga[4 * q + 2], ga[4 * q + 3]);
-                  const uint2 hub = pack4(ua[4 * q], ua[4 * q + 1], ua[4 * q + 2], ua[4 * q + 3]);
-                  const float g0 = bf16_lo(hgb.x), g1 = bf16_hi(hgb.x);
-                  const float g2 = bf16_lo(hgb.y), g3 = bf16_hi(hgb.y);
-                  const float a0 = g0 * sigmoidf_fast(g0) * bf16_lo(hub.x);
-                  const float a1 = g1 * sigmoidf_fast(g1) * bf16_hi(hub.x);
-                  const float a2 = g2 * sigmoidf_fast(g2) * bf16_lo(hub.y);
-                  const float a3 = g3 * sigmoidf_fast(g3) * bf16_hi(hub.y);
-                  *reinterpret_cast<uint2*>(g.hg + o) = hgb;
-                  *reinterpret_cast<uint2*>(g.hu + o) = hub;
-                  *reinterpret_cast<uint2*>(g.act + o) = pack4(a0, a1, a2, a3);
-                } else {
-                  const int64_t o = e * wdf + (int64_t)(m0 + m) * f + n0 + n;
-                  *reinterpret_cast<uint2*>(g.dwg + o) =
-                      pack4(ga[4 * q], ga[4 * q + 1], ga[4 * q + 2], ga[4 * q + 3]);
-                  *reinterpret_cast<uint2*>(g.dwu + o) =
-                      pack4(ua[4 * q], ua[4 * q + 1], ua[4 * q + 2], ua[4 * q + 3]);
-                }
-              }
-            });
+      const int rb = wm * 128 + 32 * i;  // tile row of the block's first row
+      if (rb >= mvalid) return;
+      if constexpr (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP) {
+        // gate [32][64] bf16 at +0, up at +4096; 128-byte rows, 16-byte chunk c of
+        // row r at c ^ ((r / 2) % 8), its 8-byte halves swapped in rows 16..31
+        // (64 banks: 32 lanes of a 64-bit write, 16 of a 128-bit read, no conflict)
+        static_for<2>([&](auto J) {
+          static_for<4>([&](auto Q) {
+            constexpr int j = J, q = Q;
+            const int off = l32 * 128 + (((4 * j + q) ^ ((l32 >> 1) & 7)) << 4) + ((lh ^ (l32 >> 4)) & 1) * 8;
+            put8(off, pack4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
+            put8(4096 + off, pack4(acc[i][j + 2][4 * q], acc[i][j + 2][4 * q + 1],
+                                   acc[i][j + 2][4 * q + 2], acc[i][j + 2][4 * q + 3]));
           });
-        } else {
-          static_for<4>([&](auto J) {
-            constexpr int j = J;
-            static_for<4>([&](auto Q) {
-              constexpr int q = Q;
-              const int n = wn * 128 + 32 * j + 8 * q + 4 * lh;
-              const float c0 = acc[i][j][4 * q], c1 = acc[i][j][4 * q + 1];
-              const float c2 = acc[i][j][4 * q + 2], c3 = acc[i][j][4 * q + 3];
-              if constexpr (MODE == FWD_DOWN) {
-                if (n0 + n < d)
-                  *reinterpret_cast<uint2*>(g.y + (int64_t)(seg + m0 + m) * d + n0 + n) =
-                      pack4(c0, c1, c2, c3);
-              } else if constexpr (MODE == DGRAD_GATE_UP) {
-                if (n0 + n < d)
-                  *reinterpret_cast<uint2*>(g.dx + (int64_t)(seg + m0 + m) * d + n0 + n) =
-                      pack4(c0, c1, c2, c3);
-              } else if constexpr (MODE == WGRAD_DOWN) {
-                if (n0 + n < d)
-                  *reinterpret_cast<uint2*>(g.dwd + e * wdf + (int64_t)(m0 + m) * d + n0 + n) =
-                      pack4(c0, c1, c2, c3);
-              } else {  // DGRAD_DOWN: SwiGLU backward
-                if (n0 + n < f) {
-                  const int64_t o = (int64_t)(seg + m0 + m) * f + n0 + n;
-                  const uint2 hgv = *reinterpret_cast<const uint2*>(g.hg_in + o);
-                  const uint2 huv = *reinterpret_cast<const uint2*>(g.hu_in + o);
-                  float dg[4], du[4], av[4];
-                  const float gz[4] = {bf16_lo(hgv.x), bf16_hi(hgv.x), bf16_lo(hgv.y),
-                                       bf16_hi(hgv.y)};
-                  const float uz[4] = {bf16_lo(huv.x), bf16_hi(huv.x), bf16_lo(huv.y),
-                                       bf16_hi(huv.y)};
-                  const float da[4] = {c0, c1, c2, c3};
-  #pragma unroll
-                  for (int u = 0; u < 4; ++u) {
-                    const float sg = sigmoidf_fast(gz[u]);
-                    const float sl = gz[u] * sg;
-                    dg[u] = da[u] * uz[u] * (sg + sl * (1.0f - sg));
-                    du[u] = da[u] * sl;
-                    av[u] = sl * uz[u];
-                  }
-                  *reinterpret_cast<uint2*>(g.dhg + o) = pack4(dg[0], dg[1], dg[2], dg[3]);
-                  *reinterpret_cast<uint2*>(g.dhu + o) = pack4(du[0], du[1], du[2], du[3]);
-                  *reinterpret_cast<uint2*>(g.act + o) = pack4(av[0], av[1], av[2], av[3]);
-                }
+        });
+        fence();
+        static_for<4>([&](auto Tt) {
+          constexpr int t = Tt;
+          const int r = 8 * t + (lane >> 3), c = lane & 7;
+          const int off = r * 128 + ((c ^ ((r >> 1) & 7)) << 4);
+          const uint4 hgv = unswap(get16(off), r), huv = unswap(get16(4096 + off), r);
+          const int rt = rb + r, col = n0 + wn * 64 + 8 * c;
+          if (rt < mvalid && col < f) {
+            if constexpr (MODE == FWD_GATE_UP) {
+              const int64_t o = (int64_t)(seg + m0 + rt) * f + col;
+              const uint32_t gw[4] = {hgv.x, hgv.y, hgv.z, hgv.w};
+              const uint32_t uw[4] = {huv.x, huv.y, huv.z, huv.w};
+              uint32_t aw[4];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                const float g0 = bf16_lo(gw[u]), g1 = bf16_hi(gw[u]);
+                aw[u] = pack_bf16x2(g0 * sigmoidf_fast(g0) * bf16_lo(uw[u]),
+                                    g1 * sigmoidf_fast(g1) * bf16_hi(uw[u]));
               }
+              *reinterpret_cast<uint4*>(g.hg + o) = hgv;
+              *reinterpret_cast<uint4*>(g.hu + o) = huv;
+              *reinterpret_cast<uint4*>(g.act + o) = make_uint4(aw[0], aw[1], aw[2], aw[3]);
+            } else {
+              const int64_t o = e * wdf + (int64_t)(m0 + rt) * f + col;
+              *reinterpret_cast<uint4*>(g.dwg + o) = hgv;
+              *reinterpret_cast<uint4*>(g.dwu + o) = huv;
+            }
+          }
+        });
+        fence();
+      } else if constexpr (MODE == DGRAD_DOWN) {
+        // SwiGLU backward from the fp32 dA block: [16][128] fp32 halves,
+        // 512-byte rows, 16-byte chunk c at c ^ row
+        static_for<2>([&](auto H) {
+          constexpr int h = H;
+          if ((l32 >> 4) == h) {
+            const int rr = l32 & 15;
+            static_for<4>([&](auto J) {
+              static_for<4>([&](auto Q) {
+                constexpr int j = J, q = Q;
+                const int c = 8 * j + 2 * q + lh;
+                put16(rr * 512 + ((c ^ rr) << 4),
+                      make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                  acc[i][j][4 * q + 3]));
+              });
             });
+          }
+          fence();
+          // SwiGLU inputs of these 16 rows: rows past the segment read as zero
+          const int cg = lane & 15;
+          const int col = n0 + wn * 128 + 8 * cg;
+          const int64_t rbase = (int64_t)(seg + m0) * f;
+          const int64_t rbytes = (int64_t)(ne - m0) * f * 2;
+          const i32x4 rhg = make_rsrc(g.hg_in + rbase, rbytes), rhu = make_rsrc(g.hu_in + rbase, rbytes);
+          uint32_t off[4];
+          static_for<4>([&](auto Tt) {
+            constexpr int t = Tt;
+            const int rt = rb + 16 * h + 4 * t + (lane >> 4);
+            off[t] = col < f ? static_cast<uint32_t>((rt * f + col) * 2) : OOB;
           });
-        }
+          u32x4a hgq[4], huq[4];
+          load_2x4_wait(rhg, rhu, off, hgq, huq);
+          uint4 hgv[4], huv[4];
+          static_for<4>([&](auto Tt) {
+            constexpr int t = Tt;
+            hgv[t] = make_uint4(hgq[t][0], hgq[t][1], hgq[t][2], hgq[t][3]);
+            huv[t] = make_uint4(huq[t][0], huq[t][1], huq[t][2], huq[t][3]);
+          });
+          static_for<4>([&](auto Tt) {
+            constexpr int t = Tt;
+            const int rr = 4 * t + (lane >> 4);
+            // chunks 2 cg and 2 cg + 1; the upper half of the lanes reads them in
+            // the other order, so that each read covers 16 distinct bank groups
+            const int ca = 2 * cg + (cg >> 3);
+            const float4 fa = getf16(rr * 512 + ((ca ^ rr) << 4));
+            const float4 fb = getf16(rr * 512 + (((ca ^ 1) ^ rr) << 4));
+            const float4 d0 = (cg >> 3) ? fb : fa, d1 = (cg >> 3) ? fa : fb;
+            const int rt = rb + 16 * h + rr;
+            {  // computed in every lane (the loads above always complete), stored where valid
+              const float da[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+              const uint32_t gw[4] = {hgv[t].x, hgv[t].y, hgv[t].z, hgv[t].w};
+              const uint32_t uw[4] = {huv[t].x, huv[t].y, huv[t].z, huv[t].w};
+              uint32_t dgw[4], duw[4], aw[4];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                float dg[2], du[2], av[2];
+#pragma unroll
+                for (int v = 0; v < 2; ++v) {
+                  const float gz = v ? bf16_hi(gw[u]) : bf16_lo(gw[u]);
+                  const float uz = v ? bf16_hi(uw[u]) : bf16_lo(uw[u]);
+                  const float sg = sigmoidf_fast(gz);
+                  const float sl = gz * sg;
+                  dg[v] = da[2 * u + v] * uz * (sg + sl * (1.0f - sg));
+                  du[v] = da[2 * u + v] * sl;
+                  av[v] = sl * uz;
+                }
+                dgw[u] = pack_bf16x2(dg[0], dg[1]);
+                duw[u] = pack_bf16x2(du[0], du[1]);
+                aw[u] = pack_bf16x2(av[0], av[1]);
+              }
+              if (rt < mvalid && col < f) {
+                const int64_t o = (int64_t)(seg + m0 + rt) * f + col;
+                *reinterpret_cast<uint4*>(g.dhg + o) = make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]);
+                *reinterpret_cast<uint4*>(g.dhu + o) = make_uint4(duw[0], duw[1], duw[2], duw[3]);
+                *reinterpret_cast<uint4*>(g.act + o) = make_uint4(aw[0], aw[1], aw[2], aw[3]);
+              }
+            }
+          });
+          fence();
+        });
+      } else {
+        // one bf16 output, [32][128] bf16, 256-byte rows, 16-byte chunk c of row r
+        // at c ^ (r % 16), its 8-byte halves swapped in rows 16..31
+        static_for<4>([&](auto J) {
+          static_for<4>([&](auto Q) {
+            constexpr int j = J, q = Q;
+            const int off = l32 * 256 + (((4 * j + q) ^ (l32 & 15)) << 4) + ((lh ^ (l32 >> 4)) & 1) * 8;
+            put8(off, pack4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
+          });
+        });
+        fence();
+        static_for<8>([&](auto Tt) {
+          constexpr int t = Tt;
+          const int r = 4 * t + (lane >> 4), c = lane & 15;
+          const uint4 v = unswap(get16(r * 256 + ((c ^ (r & 15)) << 4)), r);
+          const int rt = rb + r, col = n0 + wn * 128 + 8 * c;
+          if (rt < mvalid && col < d) {
+            uint16_t* out;
+            if constexpr (MODE == FWD_DOWN) out = g.y + (int64_t)(seg + m0 + rt) * d;
+            else if constexpr (MODE == DGRAD_GATE_UP) out = g.dx + (int64_t)(seg + m0 + rt) * d;
+            else out = g.dwd + e * wdf + (int64_t)(m0 + rt) * d;
+            *reinterpret_cast<uint4*>(out + col) = v;
+          }
+        });
+        fence();
       }
     });
   };
-
 
   // zero weight-gradient tile (expert without rows)
   auto zero_tile = [&](const Tile& tl) __attribute__((always_inline)) {
@@ -524,24 +738,44 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
     }
   };
 
-  const lds_char* ldsp = (const lds_char*)(lds);  // address-space cast
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ldsp));
+  // ------------------------------------------------------------ LDS rings
+  // NA slots of UNIT bytes for operand A, then NB for operand B.  A
+  // K-contiguous operand holds one step per slot and is loaded NA - 1 (NB - 1)
+  // steps ahead.  An N-contiguous operand is loaded by halves of 32 k: the
+  // low half of step s + NA (NB) is issued at the sync in the middle of step
+  // s, once the low half of step s has been consumed, and the high half at
+  // the sync that ends step s.  Per sync, B is issued before A.
+  constexpr bool A_K = !A_N, B_N = !B_K;
+  constexpr bool MID_SYNC = A_N || B_N;
+  constexpr int NA = 3, NB = NRING - NA;
+  constexpr int LA = A_K ? LOADS_K : LOADS_H;  // loads per wave of one issue
+  constexpr int LB = B_K ? LOADS_K : LOADS_H;
+  // Loads of this wave issued after the last one a sync needs (fixed issue
+  // order, see above): the vector-memory count each sync may leave.
+  constexpr int X_MID = (A_K && B_N) ? 24 : 20;
+  constexpr int X_END = (A_K && B_N) ? 16 : (A_K && B_K) ? 8 : 20;
+  static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
+  static_assert(LA == (A_K ? 8 : 4) && LB == (B_K ? 8 : 4) && NA == 3 && NB == 2,
+                "the sync counts above assume this ring");
+
+  lds_char* const ring = (lds_char*)(lds);  // address-space cast
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
   struct Frags {
     bf16x8 a[4], b[4];
   };
-  // fragments of half step `s` (16 k) of LDS stage `stage`
-  auto load_frags = [&](Frags& F, int stage, int s) __attribute__((always_inline)) {
-    const lds_char* ta = ldsp + stage * STAGE_BYTES;
-    const lds_char* tb = ta + OP_BYTES;
+  // fragments of sub-step `sub` (16 k, 0..3) of stream step `s`
+  auto load_frags = [&](Frags& F, int s, int sub) __attribute__((always_inline)) {
+    const lds_char* ta = ring + (s % NA) * UNIT + (A_N ? (sub >> 1) * HALF : 0);
+    const lds_char* tb = ring + (NA + s % NB) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      if constexpr (A_N) F.a[i] = AOp::frag(ta, arow[i], s, lane);
-      else F.a[i] = AOp::frag(ta, arow[i] + l32, s, lh);
+      if constexpr (A_N) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
+      else F.a[i] = AOp::frag(ta, arow[i] + l32, sub, lh);
     }
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      if constexpr (B_K) F.b[jj] = BOp::frag(tb, brow[jj] + l32, s, lh);
-      else F.b[jj] = BOp::frag(tb, brow[jj], s, lane);
+      if constexpr (B_K) F.b[jj] = BOp::frag(tb, brow[jj] + l32, sub, lh);
+      else F.b[jj] = BOp::frag(tb, brow[jj], sub & 1, lane);
     }
   };
   auto mma = [&](const Frags& F) __attribute__((always_inline)) {
@@ -551,109 +785,205 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
       for (int jj = 0; jj < 4; ++jj)
         acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[jj], F.a[i], acc[i][jj], 0, 0, 0);
   };
-  auto wait_stages = [&](int n) __attribute__((always_inline)) {  // at most n stages of this wave's loads in flight
-    if (n >= 3) wait_vmcnt<6 * LOADS>();
-    else if (n == 2) wait_vmcnt<4 * LOADS>();
-    else if (n == 1) wait_vmcnt<2 * LOADS>();
-    else wait_vmcnt<0>();
-  };
 
   // ---------------------------------------------------------- tile stream
-  // The workgroup's tiles form one stream of K steps.  Loads run up to
-  // NST steps ahead in a ring of NST LDS stages, across tile boundaries, so
-  // the next tile's first steps are in flight while the current tile
-  // finishes and writes its epilogue.  Each step is two half steps of 16 k:
-  // the fragments of the next half step are read while the MFMAs of the
-  // current one run, and the step's one barrier sits between its halves.
-  for (int i = threadIdx.x; i <= g.E_loc; i += 256) {
-    tab[i] = g.mt_start[i];
-    tab[MOE_MAX_E + 1 + i] = g.offsets[i];
-    if (i < g.E_loc) tab[2 * MOE_MAX_E + 2 + i] = g.lpt[i];
-  }
-  __syncthreads();
-  const Tables tb{tab, tab + MOE_MAX_E + 1, tab + 2 * MOE_MAX_E + 2};
-  TileIter<MODE> itc, iti;
+  // The workgroup's tiles form one stream of K steps, walked by three tile
+  // iterators: one for the MFMAs and one per operand for the loads, which
+  // run ahead across tile boundaries.  Past the end of the stream the load
+  // iterators issue the same number of loads out of range (they write zeros
+  // to slots nobody reads), which keeps every sync's count exact.  After a
+  // tile's last step its A slot (its high halves, when both operands are
+  // N-contiguous) holds the epilogue patches; the refill of that slot waits
+  // until the epilogue is done.
+  const Tables tb{g.mt_start, g.offsets, g.lpt};
+  const i32x4 nil = make_rsrc(nullptr, 0);
+  TileIter<MODE> itc, ita, itb;
   itc.init(g, tb);
-  iti.init(g, tb);
+  ita.init(g, tb);
+  itb.init(g, tb);
   zero_acc();
   Tile tc = itc.next(g, tb);
-  Tile ti = iti.next(g, tb);
   if (tc.valid) {
-    AOp A;  // operands of the tile being loaded
+    Tile tla = ita.next(g, tb), tlb = itb.next(g, tb);
+    AOp A;
     BOp B;
-    bool have = false;
-    int kti = 0, nIssued = 0;
-    auto issue_one = [&]() __attribute__((always_inline)) {
-      if (ti.valid && kti >= ti.nk) {
-        ti = iti.next(g, tb);
-        kti = 0;
-        have = false;
+    bool hava = false, havb = false;
+    int kta = 0, ktb = 0, ga = 0, gb = 0;  // step within the load tile; stream step
+    using AIssue = typename AOp::Issue;
+    using BIssue = typename BOp::Issue;
+    // h = -1: a K-contiguous unit; 0 / 1: low / high half of an N-contiguous
+    // step.  prep advances the operand's load stream by one issue and returns
+    // the issue's loads, which the caller emits (at once or between MFMAs).
+    auto prepA = [&](int h) __attribute__((always_inline)) {
+      if (h <= 0 && tla.valid && kta >= tla.nk) {
+        tla = ita.next(g, tb);
+        kta = 0;
+        hava = false;
       }
-      if (!ti.valid) return;
-      if (!have) {
-        setup(ti, A, B);
-        have = true;
+      const uint32_t base = lds0 + (ga % NA) * UNIT + (h > 0 ? HALF : 0);
+      AIssue p;
+      if (tla.valid) {
+        if (!hava) {
+          setupA(tla, A);
+          hava = true;
+        }
+        if constexpr (A_N) p = A.prep(kta, h, base, lane);
+        else p = A.prep(kta, base, lane);
+      } else {
+        p = AOp::none(nil, base);
       }
-      const uint32_t st = lds0 + (nIssued % NST) * STAGE_BYTES;
-      A.issue(kti, st, w, lane);
-      B.issue(kti, st + OP_BYTES, w, lane);
-      ++kti;
-      ++nIssued;
+      if (h != 0) {
+        ++kta;
+        ++ga;
+      }
+      return p;
     };
-#pragma unroll
-    for (int p = 0; p < NST; ++p) issue_one();
-
-    Frags cur, nxt;
-    wait_stages(nIssued - 1);
+    auto prepB = [&](int h) __attribute__((always_inline)) {
+      if (h <= 0 && tlb.valid && ktb >= tlb.nk) {
+        tlb = itb.next(g, tb);
+        ktb = 0;
+        havb = false;
+      }
+      const uint32_t base = lds0 + (NA + gb % NB) * UNIT + (h > 0 ? HALF : 0);
+      BIssue p;
+      if (tlb.valid) {
+        if (!havb) {
+          setupB(tlb, B);
+          havb = true;
+        }
+        if constexpr (B_N) p = B.prep(ktb, h, base, lane);
+        else p = B.prep(ktb, base, lane);
+      } else {
+        p = BOp::none(nil, base);
+      }
+      if (h != 0) {
+        ++ktb;
+        ++gb;
+      }
+      return p;
+    };
+    auto issueA = [&](int h) __attribute__((always_inline)) {
+      const AIssue p = prepA(h);
+      static_for<LA>([&](auto Q) { p.emit(Q, w); });
+    };
+    auto issueB = [&](int h) __attribute__((always_inline)) {
+      const BIssue p = prepB(h);
+      static_for<LB>([&](auto Q) { p.emit(Q, w); });
+    };
+    auto issue_end_b = [&]() __attribute__((always_inline)) { issueB(B_N ? 1 : -1); };
+    auto issue_end_a = [&]() __attribute__((always_inline)) { issueA(A_N ? 1 : -1); };
+    // the 16 MFMAs of one sub-step with up to 16 prepared loads between them
+    // (those of B first, then those of A: the order the sync counts assume)
+    auto mma_mix = [&](const Frags& F, const BIssue& pb, auto NBL, const AIssue& pa, auto NAL)
+        __attribute__((always_inline)) {
+      constexpr int nbl = NBL, nal = NAL;
+      static_assert(nbl + nal <= 16, "one load per MFMA at most");
+      static_for<16>([&](auto T) {
+        constexpr int t = T;
+        acc[t / 4][t % 4] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 4], F.a[t / 4], acc[t / 4][t % 4], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (t < nbl) {
+          pb.emit(t, w);
+          __builtin_amdgcn_sched_barrier(0);
+        } else if constexpr (t < nbl + nal) {
+          pa.emit(t - nbl, w);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+    };
+    // prologue: the issues the syncs of steps -3, -2, -1 would have made
+    static_for<3>([&](auto V) {
+      constexpr int v = static_cast<int>(V) - 3;
+      if constexpr (B_N && v + NB >= 0) issueB(0);
+      if constexpr (A_N && v + NA >= 0) issueA(0);
+      if constexpr (v + NB >= 0) issue_end_b();
+      if constexpr (v + NA >= 0) issue_end_a();
+    });
+    wait_vmcnt<X_END>();
+    lgkm_drained();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+
+    Frags cur, nxt;
+    int s = 0;  // stream step being computed
     load_frags(cur, 0, 0);
-    int s = 0;  // step of the stream being computed
-    bool after_epi = false;
-    // step s + 1 has landed in LDS and stage s may be refilled (barrier),
-    // then the load stream advances by one step
-    auto sync_and_issue = [&]() __attribute__((always_inline)) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave is done with stage s
-      if (after_epi) {
-        wait_vmcnt<0>();  // epilogue stores share the counter
-      } else {
-        const int later = nIssued - s - 2;  // steps issued after s + 1
-        wait_stages(later < 2 ? later : 2);
-      }
-      after_epi = false;
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      issue_one();  // into stage s % NST
+    auto sync = [&]() __attribute__((always_inline)) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
     };
-    while (true) {
-      for (int kk = 0; kk + 1 < tc.nk; ++kk) {  // all steps of the tile but its last
-        load_frags(nxt, s % NST, 1);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(cur);
-        __builtin_amdgcn_sched_barrier(0);
-        sync_and_issue();  // step s + 1 exists: it is this tile's
-        load_frags(cur, (s + 1) % NST, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(nxt);
-        __builtin_amdgcn_sched_barrier(0);
-        ++s;
-      }
-      // last step of the tile
-      load_frags(nxt, s % NST, 1);
+    // one K step; `last`: last step of the tile (its end sync defers the
+    // refill of the patch slot)
+    auto step = [&](auto LAST) __attribute__((always_inline)) {
+      constexpr bool last = LAST;
+      load_frags(nxt, s, 1);
       __builtin_amdgcn_sched_barrier(0);
       mma(cur);
       __builtin_amdgcn_sched_barrier(0);
-      const bool more = nIssued > s + 1;
-      if (more) sync_and_issue();
-      mma(nxt);
+      if constexpr (MID_SYNC) {
+        sync();
+        wait_vmcnt<X_MID>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // the low halves for later steps, spread over this sub-step's MFMAs
+        BIssue pb;
+        AIssue pa;
+        if constexpr (B_N) pb = prepB(0);
+        if constexpr (A_N) pa = prepA(0);
+        lgkm_drained();
+        load_frags(cur, s, 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_mix(nxt, pb, std::integral_constant<int, B_N ? LB : 0>{}, pa,
+                std::integral_constant<int, A_N ? LA : 0>{});
+      } else {
+        load_frags(cur, s, 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(nxt);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_frags(nxt, s, 3);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(cur);
+      __builtin_amdgcn_sched_barrier(0);
+      sync();
+      wait_vmcnt<X_END>();
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (!last) {
+        // the next step's loads, spread over the last sub-step's MFMAs
+        const BIssue pb = prepB(B_N ? 1 : -1);
+        const AIssue pa = prepA(A_N ? 1 : -1);
+        lgkm_drained();
+        load_frags(cur, s + 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_mix(nxt, pb, std::integral_constant<int, LB>{}, pa, std::integral_constant<int, LA>{});
+      } else {
+        if constexpr (A_K) issue_end_b();
+        __builtin_amdgcn_sched_barrier(0);
+        mma(nxt);
+      }
       __builtin_amdgcn_sched_barrier(0);
       ++s;
-      epilogue(tc);
+    };
+    while (true) {
+      for (int kk = 0; kk + 1 < tc.nk; ++kk) step(std::false_type{});
+      step(std::true_type{});
+      // epilogue patches: the slot(s) of the tile's last step
+      const int ls = s - 1;
+      lds_char* patch;
+      if constexpr (A_K) patch = ring + (ls % NA) * UNIT + w * PATCH_BYTES;
+      else if (w < 2) patch = ring + (ls % NA) * UNIT + HALF + w * PATCH_BYTES;
+      else patch = ring + (NA + ls % NB) * UNIT + HALF + (w - 2) * PATCH_BYTES;
+      epilogue(tc, patch);
       zero_acc();
-      after_epi = true;
-      if (!more) break;
+      wait_vmcnt<0>();  // epilogue stores share the counter with the loads
+      __builtin_amdgcn_s_barrier();  // every wave is done with its patch
+      __builtin_amdgcn_sched_barrier(0);
       tc = itc.next(g, tb);
-      load_frags(cur, s % NST, 0);  // first half of the next tile's first step
+      if (!tc.valid) break;
+      if constexpr (A_N) issue_end_b();  // the deferred refills, in sync order
+      issue_end_a();
+      lgkm_drained();
+      load_frags(cur, s, 0);
     }
   }
   if constexpr (WGRAD) {

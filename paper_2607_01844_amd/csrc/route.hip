@@ -11,73 +11,84 @@
 namespace moe {
 namespace {
 
-constexpr int KC = 32;  // hidden-index chunk staged per LDS round
-
-// Lane = expert (experts lane + 64 i, i < TE), TM tokens per wave, 4 waves
-// per block (BT = 4 TM tokens).  Per hidden index j a lane reads its TE
-// router weights (LDS, distinct per lane) and the wave's TM token values
-// (LDS broadcast, fp32), then advances TM x TE independent fma chains.
-template <int TM, int TE>
+// Lane = expert (experts lane + 64 b, b < TE); a wave owns TM tokens, a block
+// four waves.  The TM token values are uniform across the wave, so they come
+// in through scalar loads (8 bf16 per load) and feed the FMAs as scalar
+// operands; each lane reads only its own TE router weights from LDS.  W_r
+// is staged in chunks of KC hidden indices, double-buffered: the next chunk
+// is fetched into registers while the current one is consumed.
+template <int TM, int TE, int KC>
 __global__ __launch_bounds__(256) void route_logits_kernel(const uint16_t* __restrict__ x,
                                                            const float* __restrict__ w,
                                                            const float* __restrict__ bias,
                                                            int64_t T, int d, int E,
                                                            float* __restrict__ logits) {
-  constexpr int BT = 4 * TM;
-  __shared__ __align__(16) float xs[KC][BT];
-  __shared__ __align__(16) float ws[KC][64 * TE];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * BT;
+  constexpr int EW = 64 * TE;            // experts covered by one block row
+  constexpr int NW = KC * EW / 256;      // W_r values each thread stages per chunk
+  static_assert(KC % 8 == 0 && (KC * EW) % 256 == 0, "chunk shape");
+  __shared__ __align__(16) float ws[2][KC][EW];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t tw = static_cast<int64_t>(blockIdx.x) * (4 * TM) + wv * TM;
+  const uint4* xr[TM];
+#pragma unroll
+  for (int a = 0; a < TM; ++a) {
+    const int64_t t = tw + a < T ? tw + a : T - 1;  // tail rows recompute row T-1
+    xr[a] = reinterpret_cast<const uint4*>(x + t * d);
+  }
   float acc[TM][TE];
 #pragma unroll
   for (int a = 0; a < TM; ++a)
 #pragma unroll
     for (int b = 0; b < TE; ++b) acc[a][b] = +0.0f;
 
-  for (int j0 = 0; j0 < d; j0 += KC) {
-    const int kc = min(KC, d - j0);  // a multiple of 8
-    // x chunk -> fp32, transposed to [j][token]: 8 bf16 (16 bytes) per load
-    for (int q = tid; q < BT * (KC / 8); q += 256) {
-      const int tt = q / (KC / 8), jq = (q % (KC / 8)) * 8;
-      const int64_t t = t0 + tt;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (t < T && jq < kc) v = *reinterpret_cast<const uint4*>(x + t * d + j0 + jq);
-      xs[jq + 0][tt] = bf16_lo(v.x); xs[jq + 1][tt] = bf16_hi(v.x);
-      xs[jq + 2][tt] = bf16_lo(v.y); xs[jq + 3][tt] = bf16_hi(v.y);
-      xs[jq + 4][tt] = bf16_lo(v.z); xs[jq + 5][tt] = bf16_hi(v.z);
-      xs[jq + 6][tt] = bf16_lo(v.w); xs[jq + 7][tt] = bf16_hi(v.w);
+  float wr[NW];
+  auto fetch = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int q = tid + 256 * i, jj = q / EW, ee = q % EW;
+      wr[i] = (j0 + jj < d && ee < E) ? w[static_cast<int64_t>(j0 + jj) * E + ee] : 0.0f;
     }
-    // W_r chunk: KC rows x (64 TE) experts, coalesced along experts
-    for (int q = tid; q < KC * 64 * TE; q += 256) {
-      const int jj = q / (64 * TE), ee = q % (64 * TE);
-      ws[jj][ee] = (jj < kc && ee < E) ? w[static_cast<int64_t>(j0 + jj) * E + ee] : 0.0f;
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int q = tid + 256 * i;
+      ws[buf][q / EW][q % EW] = wr[i];
     }
-    __syncthreads();
-    auto step = [&](int jj) {
-      float xv[TM], wr[TE];
+  };
+  const int nch = (d + KC - 1) / KC;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    const int j0 = c * KC, kc = min(KC, d - j0);  // kc is a multiple of 8
+    if (c + 1 < nch) fetch(j0 + KC);
+    const int buf = c & 1;
+    for (int g = 0; g < kc; g += 8) {
+      uint4 xv[TM];
 #pragma unroll
-      for (int a = 0; a < TM; ++a) xv[a] = xs[jj][wv * TM + a];  // broadcast
+      for (int a = 0; a < TM; ++a) xv[a] = xr[a][(j0 + g) >> 3];  // uniform: scalar load
 #pragma unroll
-      for (int b = 0; b < TE; ++b) wr[b] = ws[jj][lane + 64 * b];
+      for (int u = 0; u < 8; ++u) {
+        float wl[TE];
 #pragma unroll
-      for (int a = 0; a < TM; ++a)
+        for (int b = 0; b < TE; ++b) wl[b] = ws[buf][g + u][lane + 64 * b];
 #pragma unroll
-        for (int b = 0; b < TE; ++b) acc[a][b] = __builtin_fmaf(xv[a], wr[b], acc[a][b]);
-    };
-    if (kc == KC) {
+        for (int a = 0; a < TM; ++a) {
+          const uint32_t pr = u < 2 ? xv[a].x : u < 4 ? xv[a].y : u < 6 ? xv[a].z : xv[a].w;
+          const float xa = (u & 1) ? bf16_hi(pr) : bf16_lo(pr);
 #pragma unroll
-      for (int jj = 0; jj < KC; ++jj) step(jj);
-    } else {
-      for (int j8 = 0; j8 < kc; j8 += 8) {
-#pragma unroll
-        for (int u = 0; u < 8; ++u) step(j8 + u);
+          for (int b = 0; b < TE; ++b) acc[a][b] = __builtin_fmaf(xa, wl[b], acc[a][b]);
+        }
       }
     }
+    if (c + 1 < nch) stash(buf ^ 1);
     __syncthreads();
   }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
-    const int64_t t = t0 + wv * TM + a;
+    const int64_t t = tw + a;
     if (t >= T) continue;
 #pragma unroll
     for (int b = 0; b < TE; ++b) {
@@ -162,21 +173,26 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
 template <int TM, int TE>
 hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                       int E, float* logits, hipStream_t s) {
+  constexpr int KC = (64 / TE) >= 8 ? (64 / TE) / 8 * 8 : 8;
   const unsigned grid = static_cast<unsigned>(ceil_div(T, 4 * TM));
   prof_begin(K_ROUTE_LOGITS, s);
-  route_logits_kernel<TM, TE><<<grid, 256, 0, s>>>(x, w, bias, T, d, E, logits);
+  route_logits_kernel<TM, TE, KC><<<grid, 256, 0, s>>>(x, w, bias, T, d, E, logits);
   prof_end(K_ROUTE_LOGITS, s);
   return hipGetLastError();
 }
 
-// Tokens per wave: the largest of 8, 4, 2 that still gives every CU a
-// workgroup.
+// Tokens per wave: the largest of 8, 4, 2, 1 that keeps TM * TE <= 32
+// chains per lane and still launches about 2048 waves (two per SIMD), so
+// that one wave's scalar-load latency is covered by the other's FMAs.
 template <int TE>
 hipError_t pick_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                        int E, float* logits, hipStream_t s) {
-  if (ceil_div(T, 32) >= 256) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
-  if (ceil_div(T, 16) >= 256) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
-  return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
+  if constexpr (TE <= 4)
+    if (T >= 8 * 2048) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
+  if constexpr (TE <= 8)
+    if (T >= 4 * 2048) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
+  if (T >= 2 * 2048) return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
+  return run_logits<1, TE>(x, w, bias, T, d, E, logits, s);
 }
 
 }  // namespace
@@ -186,11 +202,16 @@ hipError_t launch_route(const uint16_t* x, const float* w, const float* bias, in
                         hipStream_t s) {
   if (T == 0) return hipSuccess;
   hipError_t err;
-  if (E <= 64) err = pick_logits<1>(x, w, bias, T, d, E, logits, s);
-  else if (E <= 128) err = pick_logits<2>(x, w, bias, T, d, E, logits, s);
-  else if (E <= 256) err = pick_logits<4>(x, w, bias, T, d, E, logits, s);
-  else if (E <= 512) err = pick_logits<8>(x, w, bias, T, d, E, logits, s);
-  else err = pick_logits<16>(x, w, bias, T, d, E, logits, s);
+  switch ((E + 63) / 64) {
+    case 1: err = pick_logits<1>(x, w, bias, T, d, E, logits, s); break;
+    case 2: err = pick_logits<2>(x, w, bias, T, d, E, logits, s); break;
+    case 3: err = pick_logits<3>(x, w, bias, T, d, E, logits, s); break;
+    case 4: err = pick_logits<4>(x, w, bias, T, d, E, logits, s); break;
+    case 5: case 6: err = pick_logits<6>(x, w, bias, T, d, E, logits, s); break;
+    case 7: case 8: err = pick_logits<8>(x, w, bias, T, d, E, logits, s); break;
+    case 9: case 10: case 11: case 12: err = pick_logits<12>(x, w, bias, T, d, E, logits, s); break;
+    default: err = pick_logits<16>(x, w, bias, T, d, E, logits, s); break;
+  }
   if (err != hipSuccess) return err;
 
   const unsigned grid = static_cast<unsigned>(ceil_div(T, 4));
