@@ -42,10 +42,12 @@ constexpr int BN = 256;      // tile rows on the operand-B side (n)
 constexpr int BK = 64;       // k per step (128-byte rows of a K-contiguous tile)
 constexpr int UNIT = 256 * BK * 2;  // one operand tile of one step in LDS (32 KiB)
 constexpr int HALF = UNIT / 2;      // half a step (32 k) of an N-contiguous tile
-constexpr int LOADS_K = 8;   // 16-byte direct loads per lane: K-contiguous unit
-constexpr int LOADS_H = 4;   //                                N-contiguous half
+constexpr int NWAVE = 8;     // waves per workgroup: two per SIMD
+constexpr int NTHR = 64 * NWAVE;
+constexpr int LOADS_K = UNIT / 1024 / NWAVE;  // 16-byte direct loads per lane: K-contiguous unit
+constexpr int LOADS_H = HALF / 1024 / NWAVE;  //                                N-contiguous half
 constexpr int NRING = 5;     // LDS ring slots of UNIT bytes (160 KiB)
-constexpr int PATCH_BYTES = 8192;  // per-wave epilogue staging
+constexpr int PATCH_BYTES = UNIT / NWAVE;  // per-wave epilogue staging (4 KiB)
 constexpr int NXCD = 8;
 constexpr uint32_t OOB = 0x80000000u;  // buffer offset past every range: reads as zero
 
@@ -112,10 +114,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));
-// Eight 16-byte loads into registers (four from each of two buffers) that
-// complete inside the statement: the compiler never sees them in flight, so
-// its own counter bookkeeping stays exact around the K loop.  Waits for
-// every vector-memory operation of the wave.
+// Eight 16-byte loads into registers (four from each of two buffers, same
+// offsets) that complete inside the statement: the compiler never sees them
+// in flight, so its own counter bookkeeping stays exact around the K loop.
+// Waits for every vector-memory operation of the wave.
 __device__ __forceinline__ void load_2x4_wait(const i32x4& ra, const i32x4& rb, const uint32_t (&off)[4],
                                               u32x4a (&a)[4], u32x4a (&b)[4]) {
   asm volatile(
@@ -131,6 +133,37 @@ __device__ __forceinline__ void load_2x4_wait(const i32x4& ra, const i32x4& rb, 
       : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3]), "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]),
         "=&v"(b[3])
       : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(ra), "s"(rb)
+      : "memory");
+}
+// Sixteen 16-byte loads into registers (eight from each of two buffers, same
+// offsets) that complete inside the statement: the compiler never sees them
+// in flight, so its own counter bookkeeping stays exact around the K loop.
+// Waits for every vector-memory operation of the wave.
+__device__ __forceinline__ void load_2x8_wait(const i32x4& ra, const i32x4& rb, const uint32_t (&off)[8],
+                                              u32x4a (&a)[8], u32x4a (&b)[8]) {
+  asm volatile(
+      "buffer_load_dwordx4 %0, %16, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %1, %17, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %2, %18, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %3, %19, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %4, %20, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %5, %21, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %6, %22, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %7, %23, %24, 0 offen\n\t"
+      "buffer_load_dwordx4 %8, %16, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %9, %17, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %10, %18, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %11, %19, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %12, %20, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %13, %21, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %14, %22, %25, 0 offen\n\t"
+      "buffer_load_dwordx4 %15, %23, %25, 0 offen\n\t"
+      "s_waitcnt vmcnt(0)"
+      : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3]), "=&v"(a[4]), "=&v"(a[5]), "=&v"(a[6]),
+        "=&v"(a[7]), "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3]), "=&v"(b[4]), "=&v"(b[5]),
+        "=&v"(b[6]), "=&v"(b[7])
+      : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]), "v"(off[5]), "v"(off[6]),
+        "v"(off[7]), "s"(ra), "s"(rb)
       : "memory");
 }
 
@@ -431,7 +464,7 @@ struct TileIter {
 };
 
 template <int MODE>
-__global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
+__global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   __shared__ __align__(1024) char lds[NRING * UNIT];
   constexpr bool WGRAD = (MODE == WGRAD_GATE_UP || MODE == WGRAD_DOWN);
   constexpr bool DUAL = (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP);
@@ -444,7 +477,7 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
   const int64_t wdf = static_cast<int64_t>(d) * f;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w & 1, wn = w >> 1;  // 2 x 4 waves, each 128 rows x 64 columns
   const int l32 = lane & 31, lh = lane >> 5;
 
   // ------------------------------------------------------- operand setup
@@ -508,22 +541,20 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
     }
   };
 
-  int arow[4], brow[4];  // first tile row of each 32-row MFMA block
+  // First tile row of each 32-row MFMA block: four on the A side, two on
+  // the B side (dual: the gate and the up column block of the same f).
+  int arow[4], brow[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    arow[i] = wm * 128 + 32 * i;
-    if constexpr (DUAL)
-      brow[i] = (i < 2 ? 0 : BN / 2) + wn * 64 + 32 * (i & 1);
-    else
-      brow[i] = wn * 128 + 32 * i;
-  }
+  for (int i = 0; i < 4; ++i) arow[i] = wm * 128 + 32 * i;
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj) brow[jj] = DUAL ? jj * (BN / 2) + wn * 32 : wn * 64 + 32 * jj;
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
   auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
+      for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][jj][r] = 0.0f;
   };
@@ -531,12 +562,12 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
   // ------------------------------------------------------------ epilogue
   // acc[i][j][4q + u]: output row m = arow[i] + l32 (tile-relative),
   // output column n = brow[j] + 8q + 4*lh + u.  Each wave passes its
-  // 128 x 128 block through its own 8 KiB LDS patch, 32 rows (16 in fp32)
-  // at a time: it writes the accumulators in the MFMA layout and reads them
-  // back row-major, so that every global access moves 16 bytes per lane
-  // and 8 or 16 lanes cover one contiguous row segment (whole 128-byte
-  // lines instead of 32 scattered 16-byte pieces per instruction).  Patch
-  // chunks carry an XOR swizzle on the row index.
+  // 128 x 64 block through its own 4 KiB LDS patch, 32 rows (16 in fp32) at
+  // a time: it writes the accumulators in the MFMA layout and reads them
+  // back row-major, so that every global access moves 16 bytes per lane and
+  // 4 or 8 lanes cover one contiguous row segment (whole 64- or 128-byte
+  // pieces instead of 32 scattered 8-byte pieces per instruction).  Patch
+  // chunks carry XOR swizzles that keep the 64 banks conflict-free.
   auto epilogue = [&](const Tile& tl, lds_char* patch) __attribute__((always_inline)) {
     const int e = tl.e, m0 = tl.m0, n0 = tl.n0, seg = tl.seg, ne = tl.ne;
     // lane-derived indices recomputed here (not hoisted and kept live
@@ -562,6 +593,7 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
       return make_float4(v[0], v[1], v[2], v[3]);
     };
     auto fence = []() __attribute__((always_inline)) { asm volatile("" ::: "memory"); };
+    // rows 16..31 of a bf16 patch hold their two 8-byte halves swapped
     auto unswap = [](uint4 v, int r) __attribute__((always_inline)) {
       return (r & 16) ? make_uint4(v.z, v.w, v.x, v.y) : v;
     };
@@ -570,25 +602,22 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
       const int rb = wm * 128 + 32 * i;  // tile row of the block's first row
       if (rb >= mvalid) return;
       if constexpr (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP) {
-        // gate [32][64] bf16 at +0, up at +4096; 128-byte rows, 16-byte chunk c of
-        // row r at c ^ ((r / 2) % 8), its 8-byte halves swapped in rows 16..31
-        // (64 banks: 32 lanes of a 64-bit write, 16 of a 128-bit read, no conflict)
-        static_for<2>([&](auto J) {
-          static_for<4>([&](auto Q) {
-            constexpr int j = J, q = Q;
-            const int off = l32 * 128 + (((4 * j + q) ^ ((l32 >> 1) & 7)) << 4) + ((lh ^ (l32 >> 4)) & 1) * 8;
-            put8(off, pack4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
-            put8(4096 + off, pack4(acc[i][j + 2][4 * q], acc[i][j + 2][4 * q + 1],
-                                   acc[i][j + 2][4 * q + 2], acc[i][j + 2][4 * q + 3]));
-          });
+        // gate [32][32] bf16 at +0, up at +2048; 64-byte rows, 16-byte chunk c
+        // of row r at c ^ ((r / 4) % 4)
+        static_for<4>([&](auto Q) {
+          constexpr int q = Q;
+          const int off = l32 * 64 + ((q ^ ((l32 >> 2) & 3)) << 4) + ((lh ^ (l32 >> 4)) & 1) * 8;
+          put8(off, pack4(acc[i][0][4 * q], acc[i][0][4 * q + 1], acc[i][0][4 * q + 2], acc[i][0][4 * q + 3]));
+          put8(2048 + off, pack4(acc[i][1][4 * q], acc[i][1][4 * q + 1], acc[i][1][4 * q + 2],
+                                 acc[i][1][4 * q + 3]));
         });
         fence();
-        static_for<4>([&](auto Tt) {
+        static_for<2>([&](auto Tt) {
           constexpr int t = Tt;
-          const int r = 8 * t + (lane >> 3), c = lane & 7;
-          const int off = r * 128 + ((c ^ ((r >> 1) & 7)) << 4);
-          const uint4 hgv = unswap(get16(off), r), huv = unswap(get16(4096 + off), r);
-          const int rt = rb + r, col = n0 + wn * 64 + 8 * c;
+          const int r = 16 * t + (lane >> 2), c = lane & 3;
+          const int off = r * 64 + ((c ^ ((r >> 2) & 3)) << 4);
+          const uint4 hgv = unswap(get16(off), r), huv = unswap(get16(2048 + off), r);
+          const int rt = rb + r, col = n0 + wn * 32 + 8 * c;
           if (rt < mvalid && col < f) {
             if constexpr (MODE == FWD_GATE_UP) {
               const int64_t o = (int64_t)(seg + m0 + rt) * f + col;
@@ -613,57 +642,51 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
         });
         fence();
       } else if constexpr (MODE == DGRAD_DOWN) {
-        // SwiGLU backward from the fp32 dA block: [16][128] fp32 halves,
-        // 512-byte rows, 16-byte chunk c at c ^ row
+        // SwiGLU backward from the fp32 dA block, 16 rows at a time:
+        // [16][64] fp32, 256-byte rows, 16-byte chunk c of row r at c ^ r.
+        // Its inputs for the block's 32 rows come in one batch; rows past the
+        // segment read as zero.
+        const int cg = lane & 7;
+        const int col = n0 + wn * 64 + 8 * cg;
+        u32x4a hgq[4], huq[4];
+        {
+          const int64_t rbase = (int64_t)(seg + m0) * f;
+          const int64_t rbytes = (int64_t)(ne - m0) * f * 2;
+          const i32x4 rhg = make_rsrc(g.hg_in + rbase, rbytes), rhu = make_rsrc(g.hu_in + rbase, rbytes);
+          uint32_t off[4];
+          static_for<4>([&](auto Tt) {  // Tt = 2 h + t
+            constexpr int ht = Tt;
+            const int rt = rb + 16 * (ht / 2) + 8 * (ht % 2) + (lane >> 3);
+            off[ht] = col < f ? static_cast<uint32_t>((rt * f + col) * 2) : OOB;
+          });
+          load_2x4_wait(rhg, rhu, off, hgq, huq);
+        }
         static_for<2>([&](auto H) {
           constexpr int h = H;
           if ((l32 >> 4) == h) {
             const int rr = l32 & 15;
-            static_for<4>([&](auto J) {
+            static_for<2>([&](auto J) {
               static_for<4>([&](auto Q) {
                 constexpr int j = J, q = Q;
                 const int c = 8 * j + 2 * q + lh;
-                put16(rr * 512 + ((c ^ rr) << 4),
+                put16(rr * 256 + ((c ^ rr) << 4),
                       make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                                   acc[i][j][4 * q + 3]));
               });
             });
           }
           fence();
-          // SwiGLU inputs of these 16 rows: rows past the segment read as zero
-          const int cg = lane & 15;
-          const int col = n0 + wn * 128 + 8 * cg;
-          const int64_t rbase = (int64_t)(seg + m0) * f;
-          const int64_t rbytes = (int64_t)(ne - m0) * f * 2;
-          const i32x4 rhg = make_rsrc(g.hg_in + rbase, rbytes), rhu = make_rsrc(g.hu_in + rbase, rbytes);
-          uint32_t off[4];
-          static_for<4>([&](auto Tt) {
+          static_for<2>([&](auto Tt) {
             constexpr int t = Tt;
-            const int rt = rb + 16 * h + 4 * t + (lane >> 4);
-            off[t] = col < f ? static_cast<uint32_t>((rt * f + col) * 2) : OOB;
-          });
-          u32x4a hgq[4], huq[4];
-          load_2x4_wait(rhg, rhu, off, hgq, huq);
-          uint4 hgv[4], huv[4];
-          static_for<4>([&](auto Tt) {
-            constexpr int t = Tt;
-            hgv[t] = make_uint4(hgq[t][0], hgq[t][1], hgq[t][2], hgq[t][3]);
-            huv[t] = make_uint4(huq[t][0], huq[t][1], huq[t][2], huq[t][3]);
-          });
-          static_for<4>([&](auto Tt) {
-            constexpr int t = Tt;
-            const int rr = 4 * t + (lane >> 4);
-            // chunks 2 cg and 2 cg + 1; the upper half of the lanes reads them in
-            // the other order, so that each read covers 16 distinct bank groups
-            const int ca = 2 * cg + (cg >> 3);
-            const float4 fa = getf16(rr * 512 + ((ca ^ rr) << 4));
-            const float4 fb = getf16(rr * 512 + (((ca ^ 1) ^ rr) << 4));
-            const float4 d0 = (cg >> 3) ? fb : fa, d1 = (cg >> 3) ? fa : fb;
+            const int rr = 8 * t + (lane >> 3);
+            const float4 d0 = getf16(rr * 256 + (((2 * cg) ^ rr) << 4));
+            const float4 d1 = getf16(rr * 256 + (((2 * cg + 1) ^ rr) << 4));
             const int rt = rb + 16 * h + rr;
+            const u32x4a hq = hgq[2 * h + t], uq = huq[2 * h + t];
             {  // computed in every lane (the loads above always complete), stored where valid
               const float da[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-              const uint32_t gw[4] = {hgv[t].x, hgv[t].y, hgv[t].z, hgv[t].w};
-              const uint32_t uw[4] = {huv[t].x, huv[t].y, huv[t].z, huv[t].w};
+              const uint32_t gw[4] = {hq[0], hq[1], hq[2], hq[3]};
+              const uint32_t uw[4] = {uq[0], uq[1], uq[2], uq[3]};
               uint32_t dgw[4], duw[4], aw[4];
 #pragma unroll
               for (int u = 0; u < 4; ++u) {
@@ -693,21 +716,21 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
           fence();
         });
       } else {
-        // one bf16 output, [32][128] bf16, 256-byte rows, 16-byte chunk c of row r
-        // at c ^ (r % 16), its 8-byte halves swapped in rows 16..31
-        static_for<4>([&](auto J) {
+        // one bf16 output, [32][64] bf16, 128-byte rows, 16-byte chunk c of
+        // row r at c ^ ((r / 2) % 8)
+        static_for<2>([&](auto J) {
           static_for<4>([&](auto Q) {
             constexpr int j = J, q = Q;
-            const int off = l32 * 256 + (((4 * j + q) ^ (l32 & 15)) << 4) + ((lh ^ (l32 >> 4)) & 1) * 8;
+            const int off = l32 * 128 + (((4 * j + q) ^ ((l32 >> 1) & 7)) << 4) + ((lh ^ (l32 >> 4)) & 1) * 8;
             put8(off, pack4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
           });
         });
         fence();
-        static_for<8>([&](auto Tt) {
+        static_for<4>([&](auto Tt) {
           constexpr int t = Tt;
-          const int r = 4 * t + (lane >> 4), c = lane & 15;
-          const uint4 v = unswap(get16(r * 256 + ((c ^ (r & 15)) << 4)), r);
-          const int rt = rb + r, col = n0 + wn * 128 + 8 * c;
+          const int r = 8 * t + (lane >> 3), c = lane & 7;
+          const uint4 v = unswap(get16(r * 128 + ((c ^ ((r >> 1) & 7)) << 4)), r);
+          const int rt = rb + r, col = n0 + wn * 64 + 8 * c;
           if (rt < mvalid && col < d) {
             uint16_t* out;
             if constexpr (MODE == FWD_DOWN) out = g.y + (int64_t)(seg + m0 + rt) * d;
@@ -727,7 +750,7 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
     const int C = (MODE == WGRAD_GATE_UP) ? f : d;   // output columns
     const int cw = DUAL ? BN / 2 : BN;               // tile columns per output
     const int nout = DUAL ? 2 : 1;
-    for (int idx = threadIdx.x; idx < BM * (cw / 8) * nout; idx += 256) {
+    for (int idx = threadIdx.x; idx < BM * (cw / 8) * nout; idx += NTHR) {
       const int o = idx / (BM * (cw / 8));
       const int rem = idx % (BM * (cw / 8));
       const int r = tl.m0 + rem / (cw / 8), c = tl.n0 + (rem % (cw / 8)) * 8;
@@ -739,29 +762,34 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
   };
 
   // ------------------------------------------------------------ LDS rings
-  // NA slots of UNIT bytes for operand A, then NB for operand B.  A
-  // K-contiguous operand holds one step per slot and is loaded NA - 1 (NB - 1)
-  // steps ahead.  An N-contiguous operand is loaded by halves of 32 k: the
-  // low half of step s + NA (NB) is issued at the sync in the middle of step
-  // s, once the low half of step s has been consumed, and the high half at
-  // the sync that ends step s.  Per sync, B is issued before A.
+  // NA slots of UNIT bytes for operand A, then NB for operand B, one K step
+  // per slot.  One operand (F, two slots) is loaded one step ahead, the
+  // other (S, three slots) two: S is the one whose tiles miss L2 more often,
+  // the expert weights in the forward and data-gradient GEMMs.  The single
+  // sync of step s (after its last fragment reads) waits for step s + 1, then
+  // prepares F for step s + 2 and S for step s + 3, into the slots step s has
+  // freed (an N-contiguous operand as two halves of 32 k).  Their 16 loads go
+  // out between the MFMAs of the next four sub-steps (the last of step s, the
+  // first three of step s + 1), never more than six per sub-step, F's first:
+  // the memory path takes them at an even rate instead of in one burst.
   constexpr bool A_K = !A_N, B_N = !B_K;
-  constexpr bool MID_SYNC = A_N || B_N;
-  constexpr int NA = 3, NB = NRING - NA;
-  constexpr int LA = A_K ? LOADS_K : LOADS_H;  // loads per wave of one issue
-  constexpr int LB = B_K ? LOADS_K : LOADS_H;
-  // Loads of this wave issued after the last one a sync needs (fixed issue
-  // order, see above): the vector-memory count each sync may leave.
-  constexpr int X_MID = (A_K && B_N) ? 24 : 20;
-  constexpr int X_END = (A_K && B_N) ? 16 : (A_K && B_K) ? 8 : 20;
+  constexpr bool A_FIRST = !WGRAD;  // F = A (activations), S = B (weights)
+  constexpr int NA = A_FIRST ? 2 : 3, NB = NRING - NA;
+  constexpr int LA = A_K ? LOADS_K : 2 * LOADS_H;  // loads per wave of one step's issue
+  constexpr int LB = B_K ? LOADS_K : 2 * LOADS_H;
+  // Load schedule over the four sub-steps that follow a sync (see mma_mix):
+  // issue order F0, F1, S0, F2, F3, S1, S2, S3.  At the sync of step s the
+  // loads issued after the last of F(s + 1) (the later of the two it needs)
+  // are S(s + 3)'s loads 1..3: the vector-memory count it may leave.
+  constexpr int X_END = 3;
   static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
-  static_assert(LA == (A_K ? 8 : 4) && LB == (B_K ? 8 : 4) && NA == 3 && NB == 2,
-                "the sync counts above assume this ring");
+  static_assert(LA == 4 && LB == 4 && NA + NB == NRING && (NA == 2 || NB == 2),
+                "the sync count assumes this ring");
 
   lds_char* const ring = (lds_char*)(lds);  // address-space cast
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
   struct Frags {
-    bf16x8 a[4], b[4];
+    bf16x8 a[4], b[2];
   };
   // fragments of sub-step `sub` (16 k, 0..3) of stream step `s`
   auto load_frags = [&](Frags& F, int s, int sub) __attribute__((always_inline)) {
@@ -773,7 +801,7 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
       else F.a[i] = AOp::frag(ta, arow[i] + l32, sub, lh);
     }
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
+    for (int jj = 0; jj < 2; ++jj) {
       if constexpr (B_K) F.b[jj] = BOp::frag(tb, brow[jj] + l32, sub, lh);
       else F.b[jj] = BOp::frag(tb, brow[jj], sub & 1, lane);
     }
@@ -782,7 +810,7 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
+      for (int jj = 0; jj < 2; ++jj)
         acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[jj], F.a[i], acc[i][jj], 0, 0, 0);
   };
 
@@ -862,43 +890,98 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
       }
       return p;
     };
-    auto issueA = [&](int h) __attribute__((always_inline)) {
-      const AIssue p = prepA(h);
-      static_for<LA>([&](auto Q) { p.emit(Q, w); });
+    // one step's loads of an operand: a K-contiguous unit, or the two halves
+    // of an N-contiguous step
+    struct StepA {
+      AIssue p0, p1;
     };
-    auto issueB = [&](int h) __attribute__((always_inline)) {
-      const BIssue p = prepB(h);
-      static_for<LB>([&](auto Q) { p.emit(Q, w); });
+    struct StepB {
+      BIssue p0, p1;
     };
-    auto issue_end_b = [&]() __attribute__((always_inline)) { issueB(B_N ? 1 : -1); };
-    auto issue_end_a = [&]() __attribute__((always_inline)) { issueA(A_N ? 1 : -1); };
-    // the 16 MFMAs of one sub-step with up to 16 prepared loads between them
-    // (those of B first, then those of A: the order the sync counts assume)
-    auto mma_mix = [&](const Frags& F, const BIssue& pb, auto NBL, const AIssue& pa, auto NAL)
+    auto prep_stepA = [&]() __attribute__((always_inline)) {
+      StepA st;
+      if constexpr (A_N) {
+        st.p0 = prepA(0);
+        st.p1 = prepA(1);
+      } else {
+        st.p0 = prepA(-1);
+      }
+      return st;
+    };
+    auto prep_stepB = [&]() __attribute__((always_inline)) {
+      StepB st;
+      if constexpr (B_N) {
+        st.p0 = prepB(0);
+        st.p1 = prepB(1);
+      } else {
+        st.p0 = prepB(-1);
+      }
+      return st;
+    };
+    // load q (0 .. LA - 1) of a step's issue
+    auto emitA = [&](const StepA& st, int q) __attribute__((always_inline)) {
+      if constexpr (A_N) {
+        if (q < LOADS_H) st.p0.emit(q, w);
+        else st.p1.emit(q - LOADS_H, w);
+      } else {
+        st.p0.emit(q, w);
+      }
+    };
+    auto emitB = [&](const StepB& st, int q) __attribute__((always_inline)) {
+      if constexpr (B_N) {
+        if (q < LOADS_H) st.p0.emit(q, w);
+        else st.p1.emit(q - LOADS_H, w);
+      } else {
+        st.p0.emit(q, w);
+      }
+    };
+    auto issue_stepA = [&]() __attribute__((always_inline)) {
+      const StepA st = prep_stepA();
+      static_for<LA>([&](auto Q) { emitA(st, Q); });
+    };
+    auto issue_stepB = [&]() __attribute__((always_inline)) {
+      const StepB st = prep_stepB();
+      static_for<LB>([&](auto Q) { emitB(st, Q); });
+    };
+    // the 8 MFMAs of one sub-step with group G of the load schedule spread
+    // between them (group 0: F0, F1, S0; 1: F2, F3, S1; 2: S2; 3: S3)
+    auto mma_mix = [&](const Frags& F, auto G, const StepB& sb, const StepA& sa, bool pend)
         __attribute__((always_inline)) {
-      constexpr int nbl = NBL, nal = NAL;
-      static_assert(nbl + nal <= 16, "one load per MFMA at most");
-      static_for<16>([&](auto T) {
+      static_assert(LA == 4 && LB == 4, "load schedule");
+      constexpr int g = G;
+      constexpr int n = g < 2 ? 3 : 1;
+      static_for<8>([&](auto T) {
         constexpr int t = T;
-        acc[t / 4][t % 4] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 4], F.a[t / 4], acc[t / 4][t % 4], 0, 0, 0);
+        acc[t / 2][t % 2] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (t < nbl) {
-          pb.emit(t, w);
-          __builtin_amdgcn_sched_barrier(0);
-        } else if constexpr (t < nbl + nal) {
-          pa.emit(t - nbl, w);
-          __builtin_amdgcn_sched_barrier(0);
-        }
+        static_for<n>([&](auto J) {
+          constexpr int j = J;
+          if constexpr ((j * 8) / n == t) {
+            // entry: F load (first operand) or S load, with its index
+            constexpr bool is_f = g < 2 && j < 2;
+            constexpr int q = is_f ? 2 * g + j : (g < 2 ? g : g);
+            constexpr bool is_a = is_f == A_FIRST;
+            if (pend) {
+              if constexpr (is_a) emitA(sa, q);
+              else emitB(sb, q);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        });
       });
     };
     // prologue: the issues the syncs of steps -3, -2, -1 would have made
+    // (F before S)
     static_for<3>([&](auto V) {
       constexpr int v = static_cast<int>(V) - 3;
-      if constexpr (B_N && v + NB >= 0) issueB(0);
-      if constexpr (A_N && v + NA >= 0) issueA(0);
-      if constexpr (v + NB >= 0) issue_end_b();
-      if constexpr (v + NA >= 0) issue_end_a();
+      if constexpr (A_FIRST) {
+        if constexpr (v + NA >= 0) issue_stepA();
+        if constexpr (v + NB >= 0) issue_stepB();
+      } else {
+        if constexpr (v + NB >= 0) issue_stepB();
+        if constexpr (v + NA >= 0) issue_stepA();
+      }
     });
     wait_vmcnt<X_END>();
     lgkm_drained();
@@ -911,53 +994,43 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
     auto sync = [&]() __attribute__((always_inline)) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
     };
-    // one K step; `last`: last step of the tile (its end sync defers the
-    // refill of the patch slot)
+    // one K step; `last`: last step of the tile (its sync defers the refill of
+    // the patch slot).  sb / sa: the issue prepared at the previous sync,
+    // pend: whether its loads are still to go out (groups 1-3).
+    StepB sb{};
+    StepA sa{};
+    bool pend = false;
     auto step = [&](auto LAST) __attribute__((always_inline)) {
       constexpr bool last = LAST;
       load_frags(nxt, s, 1);
       __builtin_amdgcn_sched_barrier(0);
-      mma(cur);
+      mma_mix(cur, std::integral_constant<int, 1>{}, sb, sa, pend);
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (MID_SYNC) {
-        sync();
-        wait_vmcnt<X_MID>();
-        __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        // the low halves for later steps, spread over this sub-step's MFMAs
-        BIssue pb;
-        AIssue pa;
-        if constexpr (B_N) pb = prepB(0);
-        if constexpr (A_N) pa = prepA(0);
-        lgkm_drained();
-        load_frags(cur, s, 2);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_mix(nxt, pb, std::integral_constant<int, B_N ? LB : 0>{}, pa,
-                std::integral_constant<int, A_N ? LA : 0>{});
-      } else {
-        load_frags(cur, s, 2);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(nxt);
-      }
+      load_frags(cur, s, 2);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_mix(nxt, std::integral_constant<int, 2>{}, sb, sa, pend);
       __builtin_amdgcn_sched_barrier(0);
       load_frags(nxt, s, 3);
       __builtin_amdgcn_sched_barrier(0);
-      mma(cur);
+      mma_mix(cur, std::integral_constant<int, 3>{}, sb, sa, pend);
       __builtin_amdgcn_sched_barrier(0);
       sync();
       wait_vmcnt<X_END>();
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (!last) {
-        // the next step's loads, spread over the last sub-step's MFMAs
-        const BIssue pb = prepB(B_N ? 1 : -1);
-        const AIssue pa = prepA(A_N ? 1 : -1);
+        sb = prep_stepB();
+        sa = prep_stepA();
+        pend = true;
         lgkm_drained();
         load_frags(cur, s + 1, 0);
         __builtin_amdgcn_sched_barrier(0);
-        mma_mix(nxt, pb, std::integral_constant<int, LB>{}, pa, std::integral_constant<int, LA>{});
+        mma_mix(nxt, std::integral_constant<int, 0>{}, sb, sa, true);
       } else {
-        if constexpr (A_K) issue_end_b();
+        // F goes out now; S's refill would land in the epilogue patches
+        if constexpr (A_FIRST) issue_stepA();
+        else issue_stepB();
+        pend = false;
         __builtin_amdgcn_sched_barrier(0);
         mma(nxt);
       }
@@ -967,12 +1040,10 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
     while (true) {
       for (int kk = 0; kk + 1 < tc.nk; ++kk) step(std::false_type{});
       step(std::true_type{});
-      // epilogue patches: the slot(s) of the tile's last step
+      // epilogue patches: S's slot of the tile's last step
       const int ls = s - 1;
-      lds_char* patch;
-      if constexpr (A_K) patch = ring + (ls % NA) * UNIT + w * PATCH_BYTES;
-      else if (w < 2) patch = ring + (ls % NA) * UNIT + HALF + w * PATCH_BYTES;
-      else patch = ring + (NA + ls % NB) * UNIT + HALF + (w - 2) * PATCH_BYTES;
+      lds_char* const patch =
+          ring + (A_FIRST ? (NA + ls % NB) : (ls % NA)) * UNIT + w * PATCH_BYTES;
       epilogue(tc, patch);
       zero_acc();
       wait_vmcnt<0>();  // epilogue stores share the counter with the loads
@@ -980,8 +1051,8 @@ __global__ __launch_bounds__(256, 1) void grouped_gemm_kernel(GemmArgs g) {
       __builtin_amdgcn_sched_barrier(0);
       tc = itc.next(g, tb);
       if (!tc.valid) break;
-      if constexpr (A_N) issue_end_b();  // the deferred refills, in sync order
-      issue_end_a();
+      if constexpr (A_FIRST) issue_stepB();  // S's deferred refill
+      else issue_stepA();
       lgkm_drained();
       load_frags(cur, s, 0);
     }
@@ -1058,7 +1129,7 @@ template <int MODE>
 hipError_t run_gemm(const GemmArgs& a, int64_t blocks, int kid, hipStream_t s) {
   if (blocks <= 0) return hipSuccess;
   prof_begin(kid, s);
-  grouped_gemm_kernel<MODE><<<static_cast<unsigned>(blocks), 256, 0, s>>>(a);
+  grouped_gemm_kernel<MODE><<<static_cast<unsigned>(blocks), NTHR, 0, s>>>(a);
   prof_end(kid, s);
   return hipGetLastError();
 }
