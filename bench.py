@@ -117,6 +117,37 @@ def kernel_table(wl, M, T_touched, prof, steps):
     return rows, flops, bytes_
 
 
+TRAFFIC_SOURCES = ("paper_2607_01844_amd/csrc/gemm.hip", "paper_2607_01844_amd/csrc/common.h")
+
+
+def stored_traffic(workload: str, kernel: str):
+    """HBM-side bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE / WRITE_SIZE passes scaled by a plain copy of known size), or
+    None when there is no summary for this workload or the kernel sources have
+    changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"moe_layer_{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    h = hashlib.sha256()
+    for p in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as fh:
+            h.update(fh.read())
+    src, found = None, None
+    with open(path) as fh:
+        for line in fh:
+            f = line.split()
+            if not f or f[0].startswith("#"):
+                continue
+            if f[0] == "source_sha256":
+                src = f[1]
+            elif f[0] == "kernel" and f[1] == kernel:
+                found = {kv.split("=")[0]: int(kv.split("=")[1]) for kv in f[2:]}
+    if src != h.hexdigest() or found is None:
+        return None
+    return found["read_bytes"] + found["write_bytes"]
+
+
 def cpu_baseline(wl, inp, budget_s: float):
     """The oracle (as is) on the first T_s tokens of the same workload."""
     import oracle
@@ -207,7 +238,8 @@ def main():
         ach = flops[dom] / avg_s / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                "traffic": None, "avg_us": round(avg_s * 1e6, 2),
+                "traffic": stored_traffic(wl.name, dom), "traffic_unit": "bytes per launch",
+                "avg_us": round(avg_s * 1e6, 2),
                 "work_per_launch": f"{flops[dom]:.4g} FLOP"}
         log(f"[bench] grouped GEMMs {gemm_tflops:.0f} TFLOP/s; dominant {dom} {ach:.0f} TFLOP/s")
 
