@@ -4,7 +4,8 @@ One step = the whole hot path over one batch of synthetic input, all through
 the C ABI on one stream: route -> permute -> grouped SwiGLU forward ->
 combine -> combine backward -> grouped SwiGLU backward (data and weight
 gradients) -> permutation backward.  Inputs are resident in HBM before the
-timed region starts.
+timed region starts.  A second timed loop adds the router backward (dW_r,
+dbias and the router's share of dx) to every step: "with_router_backward".
 
 Prints ONE JSON line (rank 0).  Default workload: T=4096 tokens, d=2048,
 E=64 experts, top-6, f=1408 SwiGLU (bf16, fp32 router, seed 0).
@@ -54,6 +55,7 @@ class Layer:
         self.dxp, self.dx = e(cap, d), e(T, d)
         self.dwg, self.dwu = torch.empty_like(inp["w_gate"]), torch.empty_like(inp["w_up"])
         self.dwd = torch.empty_like(inp["w_down"])
+        self.dwr = e(d, wl.E, dt=torch.float32)
         self.pm = None
 
     def step(self):
@@ -73,6 +75,13 @@ class Layer:
                                  inp["w_up"], inp["w_down"], cap=wl.cap, dx_perm=self.dxp,
                                  dw_gate=self.dwg, dw_up=self.dwu, dw_down=self.dwd)
         m.moe_combine(self.dxp, pm["dst"], None, out=self.dx)
+
+    def router_bwd(self):
+        """The router's gradient (dW_r, dbias) and its share of dx, added in place."""
+        m, wl, inp = self.moe, self.wl, self.inp
+        m.moe_route_bwd(inp["x"], inp["w_router"], self.logits, self.idx, self.gate, self.dgate,
+                        wl.renorm, dx=self.dx, dx_accumulate=True,
+                        with_dbias=inp["router_bias"] is not None, dw_router=self.dwr)
 
     def _permute_into(self):
         # reuse the permutation buffers of the first step (no allocation)
@@ -96,7 +105,8 @@ def kernel_table(wl, M, T_touched, prof, steps):
     flops = {"gemm_fwd_gate_up": 4.0 * M * d * f, "gemm_fwd_down": 2.0 * M * d * f,
              "gemm_dgrad_down": 2.0 * M * d * f, "gemm_dgrad_gate_up": 4.0 * M * d * f,
              "gemm_wgrad_gate_up": 4.0 * M * d * f, "gemm_wgrad_down": 2.0 * M * d * f,
-             "route_logits": 2.0 * T * d * wl.E}
+             "route_logits": 2.0 * T * d * wl.E, "route_dw": 2.0 * T * d * wl.E,
+             "route_dx": 2.0 * T * d * wl.E}
     # combine runs twice per step (weighted forward, unit-weight permute backward)
     comb = 0.5 * ((M * d * 2 + T * d * 2 + T * k * 8) + (M * d * 2 + T * d * 2 + T * k * 4))
     bytes_ = {"permute_gather": T_touched * d * 2 + M * d * 2 + T * k * 4,
@@ -213,6 +223,17 @@ def main():
     tok_s = wl.T / (ms * 1e-3)
     log(f"[bench] {ms:.3f} ms/step, {tok_s:.0f} tokens/s")
 
+    # the same step followed by the router backward (whole-layer dx, dW_r)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        layer.step()
+        layer.router_bwd()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_rb = start.elapsed_time(stop) / args.steps
+    log(f"[bench] with router backward {ms_rb:.3f} ms/step")
+
     off = layer.pm["expert_offsets"].cpu().numpy()
     M = int(off[-1])
     cnt = np.diff(off)
@@ -226,6 +247,7 @@ def main():
         m.profile_enable(True)
         for _ in range(args.steps):
             layer.step()
+            layer.router_bwd()
         torch.cuda.synchronize()
         m.profile_enable(False)
         prof = m.profile_query()
@@ -267,6 +289,8 @@ def main():
         "grouped_gemm_tflops": None if gemm_tflops is None else round(gemm_tflops, 1),
         "grouped_gemm_frac_bf16_peak": None if gemm_tflops is None
         else round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
+        "with_router_backward": {"ms_per_step": round(ms_rb, 4),
+                                 "value": round(wl.T / (ms_rb * 1e-3), 1), "unit": "tokens/s"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,

@@ -25,8 +25,9 @@
  *    on the host before any HIP call; on MOE_ERR_INVALID_ARG or
  *    MOE_ERR_WORKSPACE nothing was enqueued and outputs are untouched.
  *    moe_last_error() returns a message for the calling thread's last error.
- *  - Outputs must not alias inputs.  Results are bitwise deterministic run to
- *    run (no floating-point atomics).
+ *  - Outputs must not alias inputs (moe_route_bwd's dx, updated in place, is
+ *    the one exception).  Results are bitwise deterministic run to run (no
+ *    floating-point atomics).
  *  - cap >= T * min(k, num_local) is the row capacity of permuted buffers;
  *    rows [M, cap) of them are never read and are left unspecified.
  *  - Limits: 1 <= k <= MOE_MAX_K, k <= E <= MOE_MAX_E, T >= 0,
@@ -88,6 +89,39 @@ int moe_route_workspace_bytes(int64_t T, int E, size_t* bytes);
 int moe_route(const moe_bf16* x, const float* w_router, const float* router_bias, int64_t T,
               int d, int E, int k, int renorm, int32_t* topk_idx, float* topk_gate,
               float* logits, void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------- router backward
+ * Gradient of the router (a dense weight, Sec. 3.1 eq. (param-decomp)) from
+ * the gate gradients that moe_combine_bwd returns.  With s = sum_i dgate[t][i]
+ * gate[t][i] (i ascending), the logit gradient is
+ *   renorm = 0: dlogits[t][e] = -p_e s + sum over slots i with topk_idx = e of
+ *               dgate[t][i] gate[t][i], p = softmax of logits[t] over all E;
+ *   renorm = 1: dlogits[t][topk_idx[t][i]] = gate[t][i] (dgate[t][i] - s),
+ *               0 for experts not chosen.
+ * Then, all in fp32 with fixed summation orders (bitwise reproducible):
+ *   dw_router[j][e] = sum over t of float(x[t][j]) dlogits[t][e]   (overwritten)
+ *   dbias[e]        = sum over t of dlogits[t][e]                  (optional)
+ *   dx[t][j]        = bf16( [float(dx[t][j]) +] sum over e ascending of
+ *                     dlogits[t][e] w_router[j][e] )               (optional)
+ * dx_accumulate = 1 adds the router's share to the expert path's input
+ * gradient already in dx (e.g. from the unit-weight moe_combine of dx_perm),
+ * giving the whole layer's dx; dx is then read and written in place (the one
+ * allowed alias).  dx_accumulate = 0 writes the router's share alone.
+ *
+ * x [T][d] bf16; w_router [d][E] fp32; logits [T][E] fp32 (as moe_route
+ * wrote them); topk_idx, topk_gate, dgate [T][k]; dw_router [d][E] fp32;
+ * dbias [E] fp32 or NULL; dx [T][d] bf16 or NULL; dlogits [T][E] fp32 or
+ * NULL (then kept in the workspace).  The workspace must hold
+ * moe_route_bwd_workspace_bytes(), less the T*E*4 bytes of dlogits (rounded
+ * up to 256) when dlogits is given; it may be NULL when that leaves 0.
+ * T = 0 is valid: dw_router and dbias become exact zeros.
+ */
+int moe_route_bwd_workspace_bytes(int64_t T, int d, int E, size_t* bytes);
+int moe_route_bwd(const moe_bf16* x, const float* w_router, const float* logits,
+                  const int32_t* topk_idx, const float* topk_gate, const float* dgate,
+                  int64_t T, int d, int E, int k, int renorm, float* dw_router, float* dbias,
+                  moe_bf16* dx, int dx_accumulate, float* dlogits, void* workspace,
+                  size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------- permutation
  * Group this device's token-expert assignments into contiguous per-expert

@@ -71,6 +71,7 @@ def _declare(L):
         "oracle_combine_bwd_f64_bf16": [_P, _P, _P, _P, _I64, _I, _I, _P, _P],
         "oracle_combine_bwd_f64_f64": [_P, _P, _P, _P, _I64, _I, _I, _P, _P],
         "oracle_router_bwd_f64": [_P, _P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P, _P, _P],
+        "oracle_router_dlogits_f64": [_P, _P, _P, _P, _I64, _I, _I, _I, _P],
     }
     for suf in ("f32_bf16", "f64_bf16", "f64_f64"):
         sig["oracle_ffn_fwd_rows_" + suf] = [_P, _P, _I64, _I, _I, _P, _P, _P, _P, _P, _P, _P]
@@ -254,6 +255,33 @@ def router_bwd_f64(x, w_r, lg, idx, gate, dgate, renorm=0):
     dw = np.empty((d, E)); dx = np.empty((T, d)); db = np.empty(E)
     lib().oracle_router_bwd_f64(_ptr(x), _ptr(w_r), _ptr(lg), _ptr(idx), _ptr(gate),
                                 _ptr(dgate), T, d, E, k, renorm, _ptr(dw), _ptr(dx), _ptr(db))
+    return dw, dx, db
+
+
+def router_dlogits_f64(lg, idx, gate, dgate, renorm=0):
+    """Logit gradients from gate gradients (the softmax Jacobian at the chosen
+    slots; the router of Sec. 2.1 is a dense weight, Sec. 3.1), fp64."""
+    lg, gate, dgate = (_c(v, np.float64) for v in (lg, gate, dgate))
+    idx = _c(idx, np.int32)
+    T, E = lg.shape
+    k = idx.shape[1]
+    dl = np.empty((T, E))
+    lib().oracle_router_dlogits_f64(_ptr(lg), _ptr(idx), _ptr(gate), _ptr(dgate), T, E, k,
+                                    renorm, _ptr(dl))
+    return dl
+
+
+def router_bwd_entries_f64(x, w_r, dl, jj, ee, tt):
+    """Selected outputs of the router backward, by definition, in fp64:
+    dW_r[jj[n], ee[n]] = sum_t x[t, jj[n]] dl[t, ee[n]], the router's input
+    gradient rows dx[tt[m], :] = dl[tt[m], :] W_r^T (one dot product each) and
+    the bias gradient sum_t dl[t, :]."""
+    x = np.asarray(x, np.float64)
+    w_r = np.asarray(w_r, np.float64)
+    dl = np.asarray(dl, np.float64)
+    dw = np.array([np.dot(x[:, j], dl[:, e]) for j, e in zip(jj, ee)])
+    dx = np.array([[np.dot(dl[t], w_r[j]) for j in range(w_r.shape[0])] for t in tt])
+    db = np.array([np.sum(dl[:, e]) for e in range(dl.shape[1])])
     return dw, dx, db
 
 

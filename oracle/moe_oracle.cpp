@@ -397,13 +397,12 @@ ORACLE_COMBINE_BWD(oracle_combine_bwd_f64_f64, double, double, double)
 // From dgate to d logits (softmax Jacobian at the chosen slots), then
 // dW_r = x^T dlogits and dx_router = dlogits W_r^T.  The bias gradient is
 // sum_t dlogits[t] (returned when dbias != NULL).
-void oracle_router_bwd_f64(const double* x, const double* w_r, const double* logits,
-                           const int32_t* idx, const double* gate, const double* dgate,
-                           int64_t T, int d, int E, int k, int renorm, double* dw_r,
-                           double* dx, double* dbias) {
-  std::vector<double> dl(static_cast<size_t>(T) * E, 0.0);
+void oracle_router_dlogits_f64(const double* logits, const int32_t* idx, const double* gate,
+                               const double* dgate, int64_t T, int E, int k, int renorm,
+                               double* dl) {
+  for (int64_t i = 0; i < T * E; ++i) dl[i] = 0.0;
   for (int64_t t = 0; t < T; ++t) {
-    double* g = dl.data() + t * E;
+    double* g = dl + t * E;
     if (renorm == 0) {
       // gate_i = p[e_i], p = softmax(l):  dl_e = sum_i dgate_i p_{e_i} (delta - p_e)
       double m = logits[t * E];
@@ -421,6 +420,14 @@ void oracle_router_bwd_f64(const double* x, const double* w_r, const double* log
       for (int i = 0; i < k; ++i) g[idx[t * k + i]] = gate[t * k + i] * (dgate[t * k + i] - s);
     }
   }
+}
+
+void oracle_router_bwd_f64(const double* x, const double* w_r, const double* logits,
+                           const int32_t* idx, const double* gate, const double* dgate,
+                           int64_t T, int d, int E, int k, int renorm, double* dw_r,
+                           double* dx, double* dbias) {
+  std::vector<double> dl(static_cast<size_t>(T) * E, 0.0);
+  oracle_router_dlogits_f64(logits, idx, gate, dgate, T, E, k, renorm, dl.data());
   for (int j = 0; j < d; ++j)
     for (int e = 0; e < E; ++e) {
       double s = 0.0;

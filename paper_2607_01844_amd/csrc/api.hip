@@ -86,7 +86,8 @@ const char* const kNames[moe::K_NUM] = {
     "route_logits", "route_topk",      "permute_count",      "permute_scan",
     "permute_rank", "permute_gather",  "gemm_sched",         "gemm_fwd_gate_up",
     "gemm_fwd_down", "gemm_dgrad_down", "gemm_dgrad_gate_up", "gemm_wgrad_gate_up",
-    "gemm_wgrad_down", "combine",       "combine_bwd"};
+    "gemm_wgrad_down", "combine",       "combine_bwd",        "route_dlogits",
+    "route_dw",     "route_dx"};
 
 }  // namespace
 
@@ -157,6 +158,44 @@ MOE_API int moe_route(const moe_bf16* x, const float* w_router, const float* rou
   }
   return hip_status(moe::launch_route(x, w_router, router_bias, T, d, E, k, renorm, topk_idx,
                                       topk_gate, lg, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+MOE_API int moe_route_bwd_workspace_bytes(int64_t T, int d, int E, size_t* bytes) {
+  const char* fn = "moe_route_bwd_workspace_bytes";
+  CHECK(bytes != nullptr, "bytes is NULL");
+  CHECK(T >= 0 && E >= 1 && E <= MOE_MAX_E, "bad T or E");
+  if (int r = check_dim(fn, d, "d")) return r;
+  *bytes = moe::route_bwd_ws_bytes(T, d, E);
+  return MOE_OK;
+}
+
+MOE_API int moe_route_bwd(const moe_bf16* x, const float* w_router, const float* logits,
+                          const int32_t* topk_idx, const float* topk_gate, const float* dgate,
+                          int64_t T, int d, int E, int k, int renorm, float* dw_router,
+                          float* dbias, moe_bf16* dx, int dx_accumulate, float* dlogits,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "moe_route_bwd";
+  if (int r = check_tk(fn, T, E, k)) return r;
+  if (int r = check_dim(fn, d, "d")) return r;
+  CHECK(renorm == 0 || renorm == 1, "renorm must be 0 or 1");
+  CHECK(dx_accumulate == 0 || dx_accumulate == 1, "dx_accumulate must be 0 or 1");
+  REQ(dw_router);
+  OPT(dbias);
+  if (T > 0) {
+    REQ(x); REQ(w_router); REQ(logits); REQ(topk_idx); REQ(topk_gate); REQ(dgate);
+    OPT(dx); OPT(dlogits);
+  }
+  size_t need = moe::route_bwd_ws_bytes(T, d, E);
+  if (dlogits != nullptr) need -= moe::align_up(sizeof(float) * static_cast<size_t>(T) * E, 256);
+  if (need > 0) {
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(MOE_ERR_WORKSPACE, fn, "workspace smaller than moe_route_bwd_workspace_bytes()");
+    OPT(workspace);
+  }
+  return hip_status(moe::launch_route_bwd(x, w_router, logits, topk_idx, topk_gate, dgate, T, d,
+                                          E, k, renorm, dw_router, dbias, dx, dx_accumulate,
+                                          dlogits, workspace, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

@@ -80,6 +80,9 @@ enum KernelId {
   K_GEMM_WGRAD_DOWN,
   K_COMBINE,
   K_COMBINE_BWD,
+  K_ROUTE_DLOGITS,
+  K_ROUTE_DW,
+  K_ROUTE_DX,
   K_NUM
 };
 
@@ -95,6 +98,13 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 hipError_t launch_route(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                         int E, int k, int renorm, int32_t* idx, float* gate, float* logits,
                         hipStream_t s);
+int route_bwd_chunks(int64_t T, int d, int E);
+size_t route_bwd_ws_bytes(int64_t T, int d, int E);
+hipError_t launch_route_bwd(const uint16_t* x, const float* w, const float* logits,
+                            const int32_t* idx, const float* gate, const float* dgate,
+                            int64_t T, int d, int E, int k, int renorm, float* dw, float* dbias,
+                            uint16_t* dx, int dx_accumulate, float* dlogits, void* ws,
+                            hipStream_t s);
 size_t permute_ws_bytes(int64_t T, int E, int k, int E_loc);
 hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int d, int E, int k,
                           int e_begin, int E_loc, int32_t* offsets, int32_t* counts_global,

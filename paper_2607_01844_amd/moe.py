@@ -25,6 +25,7 @@ MOE_MAX_E = 1024
 C_SYMBOLS = (
     "moe_abi_version", "moe_status_string", "moe_last_error",
     "moe_route_workspace_bytes", "moe_route",
+    "moe_route_bwd_workspace_bytes", "moe_route_bwd",
     "moe_permute_workspace_bytes", "moe_permute",
     "moe_grouped_swiglu_workspace_bytes", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
     "moe_combine", "moe_combine_bwd",
@@ -51,6 +52,8 @@ def _load():
         "moe_last_error": ([], ctypes.c_char_p),
         "moe_route_workspace_bytes": ([I64, I, PSZ], I),
         "moe_route": ([P, P, P, I64, I, I, I, I, P, P, P, P, SZ, P], I),
+        "moe_route_bwd_workspace_bytes": ([I64, I, I, PSZ], I),
+        "moe_route_bwd": ([P, P, P, P, P, P, I64, I, I, I, I, P, P, P, I, P, P, SZ, P], I),
         "moe_permute_workspace_bytes": ([I64, I, I, I, PSZ], I),
         "moe_permute": ([P, P, I64, I, I, I, I, I, P, P, P, P, P, P, SZ, P], I),
         "moe_grouped_swiglu_workspace_bytes": ([I64, I, I, I, U, PSZ], I),
@@ -143,6 +146,44 @@ def moe_route(x, w_router, router_bias, k, renorm=0, logits=None, topk_idx=None,
                          _ptr(topk_idx), _ptr(topk_gate), _ptr(logits), _ptr(ws), nws, _stream()),
            "moe_route")
     return topk_idx, topk_gate
+
+
+def moe_route_bwd(x, w_router, logits, topk_idx, topk_gate, dgate, renorm=0, dx=None,
+                  dx_accumulate=True, with_dbias=False, dlogits=None, dw_router=None):
+    """Router gradient from the gate gradients.
+
+    Returns (dw_router [d,E] fp32, dbias [E] fp32 or None, dx or None).  When
+    dx is given it is updated in place (dx_accumulate) or overwritten with the
+    router's share of the input gradient.
+    """
+    _need(x, torch.bfloat16, "x", 2)
+    _need(w_router, torch.float32, "w_router", 2)
+    _need(logits, torch.float32, "logits", 2)
+    _need(topk_idx, torch.int32, "topk_idx", 2)
+    _need(topk_gate, torch.float32, "topk_gate", 2)
+    _need(dgate, torch.float32, "dgate", 2)
+    if dx is not None:
+        _need(dx, torch.bfloat16, "dx", 2)
+    if dlogits is not None:
+        _need(dlogits, torch.float32, "dlogits", 2)
+    T, d = x.shape
+    E = w_router.shape[1]
+    k = topk_idx.shape[1]
+    dev = x.device
+    if dw_router is None:
+        dw_router = torch.empty((d, E), dtype=torch.float32, device=dev)
+    else:
+        _need(dw_router, torch.float32, "dw_router", 2)
+    dbias = torch.empty((E,), dtype=torch.float32, device=dev) if with_dbias else None
+    n = ctypes.c_size_t()
+    _check(lib.moe_route_bwd_workspace_bytes(T, d, E, ctypes.byref(n)),
+           "moe_route_bwd_workspace_bytes")
+    ws = workspace(n.value, dev, "route_bwd")
+    _check(lib.moe_route_bwd(_ptr(x), _ptr(w_router), _ptr(logits), _ptr(topk_idx),
+                             _ptr(topk_gate), _ptr(dgate), T, d, E, k, renorm, _ptr(dw_router),
+                             _ptr(dbias), _ptr(dx), 1 if dx_accumulate else 0, _ptr(dlogits),
+                             _ptr(ws), ws.numel(), _stream()), "moe_route_bwd")
+    return dw_router, dbias, dx
 
 
 # ------------------------------------------------------------ permutation

@@ -345,3 +345,27 @@ def test_workload_generator_is_seeded():
         assert np.array_equal(a[key].float().numpy(), b[key].float().numpy()), key
     wl = W.WORKLOADS["tiny"]
     assert a["x"].shape == (wl.T, wl.d) and a["w_down"].shape == (wl.E_loc, wl.f, wl.d)
+
+
+def test_router_backward_entries_agree_with_full(orc):
+    """The sampled router-backward helper (dot products in numpy) agrees with
+    the full C routine (loops), which the finite-difference test pins."""
+    rng = np.random.default_rng(7)
+    T, d, E, k = 40, 24, 9, 3
+    x = rng.normal(size=(T, d))
+    w = 0.3 * rng.normal(size=(d, E))
+    lg = x @ w
+    idx, gate = orc.topk(lg, k, 0)
+    dg = rng.normal(size=(T, k))
+    for renorm in (0, 1):
+        idx, gate = orc.topk(lg, k, renorm)
+        dw, dx, db = orc.router_bwd_f64(x, w, lg, idx, gate, dg, renorm)
+        dl = orc.router_dlogits_f64(lg, idx, gate, dg, renorm)
+        jj, ee, tt = [0, 5, 23], [8, 0, 4], [0, 17, 39]
+        dw_s, dx_s, db_s = orc.router_bwd_entries_f64(x, w, dl, jj, ee, tt)
+        assert np.allclose(dw_s, dw[jj, ee], rtol=0, atol=1e-12)
+        assert np.allclose(dx_s, dx[tt], rtol=0, atol=1e-12)
+        assert np.allclose(db_s, db, rtol=0, atol=1e-12)
+        # the logit gradients of one token sum to zero under renorm = 0 and 1
+        # (softmax is invariant to a common shift of its logits)
+        assert np.allclose(dl.sum(1), 0.0, atol=1e-12)
