@@ -333,7 +333,8 @@ struct GemmArgs {
   const uint16_t* dhu_in;
   const int32_t* offsets;   // [E_loc+1]
   const int32_t* mt_start;  // [E_loc+1] prefix of per-expert row-tile counts
-  const int32_t* lpt;       // [E_loc] experts by rows, descending
+  const int32_t* wk_start;  // [E_loc+1] prefix of per-expert K steps (weight gradients)
+  const int32_t* nz_start;  // [E_loc+1] prefix of the count of experts with rows
   // outputs
   uint16_t* hg;
   uint16_t* hu;
@@ -370,10 +371,12 @@ struct Tile {
 //  * Row-grouped GEMMs: logical tiles (expert-major; inside an expert the
 //    row tiles of one column tile are adjacent) are cut into 8 equal
 //    contiguous ranges, one per XCD, dealt round-robin to the XCD's CUs.
-//  * Weight gradients: groups (expert, row tile) in LPT order (experts by
-//    rows, descending) are dealt to XCDs in snake order (0..7, 7..0, ...),
-//    which balances skewed loads and spreads a large expert over all XCDs;
-//    the column tiles of a group are adjacent on its XCD.
+//  * Weight gradients: every expert with rows has MT x NT tiles of K = its
+//    row count; the tiles (expert-major, row tiles of one column tile
+//    adjacent) are cut into 8 contiguous ranges of equal K-step work, one per
+//    XCD, dealt round-robin to the XCD's CUs.  An expert's tiles thus share
+//    one L2 (its activations and gradient rows are fetched once per XCD)
+//    unless it is larger than an XCD's share.
 // Schedule tables of one launch, read with scalar loads: tile decoding is
 // uniform, and a scalar load waits on the LDS/scalar counter only, never on
 // the vector-memory counter that tracks the operand loads in flight.
@@ -385,10 +388,12 @@ __device__ __forceinline__ int sld(const int32_t* p) {
 struct Tables {
   const int32_t* mt_start_;  // [E_loc + 1]
   const int32_t* offsets_;   // [E_loc + 1]
-  const int32_t* lpt_;       // [E_loc]
+  const int32_t* wk_start_;  // [E_loc + 1]
+  const int32_t* nz_start_;  // [E_loc + 1]
   __device__ __forceinline__ int mt(int i) const { return sld(mt_start_ + i); }
   __device__ __forceinline__ int off(int i) const { return sld(offsets_ + i); }
-  __device__ __forceinline__ int lpt(int i) const { return sld(lpt_ + i); }
+  __device__ __forceinline__ int wk(int i) const { return sld(wk_start_ + i); }
+  __device__ __forceinline__ int nz(int i) const { return sld(nz_start_ + i); }
 };
 
 template <int MODE>
@@ -397,8 +402,23 @@ struct TileIter {
   static constexpr bool DUAL = (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP);
   int xcd, j, cpx, i;
   int total, end;  // row-grouped: tile count, end of this XCD's range
-  int gq, lim;     // weight gradients: group count, XCD-local tile bound
+  int unit;        // weight gradients: tiles per expert with rows (MT * NT)
+  int ecache;      // weight gradients: expert of the previous tile
   bool zeros;      // weight gradients: visit only the tiles of experts without rows
+
+  // Weight gradients: first tile whose K-step work starts at or after `b`.
+  __device__ __forceinline__ int wg_tile_at(const GemmArgs& g, const Tables& tb, int64_t b) const {
+    const int64_t W = static_cast<int64_t>(unit) * tb.wk(g.E_loc);
+    if (b >= W) return unit * tb.nz(g.E_loc);
+    int lo = 0, hi = g.E_loc - 1;  // smallest e with unit * wk(e + 1) > b
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (static_cast<int64_t>(unit) * tb.wk(mid + 1) > b) hi = mid; else lo = mid + 1;
+    }
+    const int64_t w0 = static_cast<int64_t>(unit) * tb.wk(lo);
+    const int nk = tb.wk(lo + 1) - tb.wk(lo);
+    return unit * tb.nz(lo) + static_cast<int>((b - w0 + nk - 1) / nk);
+  }
 
   __device__ __forceinline__ void init(const GemmArgs& g, const Tables& tb, bool zero_tiles = false) {
     zeros = zero_tiles;
@@ -411,9 +431,12 @@ struct TileIter {
       const int per = (total + NXCD - 1) / NXCD;
       end = min((xcd + 1) * per, total);
       total = xcd * per;  // start of this XCD's range
-    } else {
-      gq = g.E_loc * g.MT;
-      lim = 2 * ((gq + 15) / 16) * g.NT;
+    } else if (!zero_tiles) {
+      unit = g.MT * g.NT;
+      ecache = 0;
+      const int64_t W = static_cast<int64_t>(unit) * tb.wk(g.E_loc);
+      total = wg_tile_at(g, tb, W * xcd / NXCD);
+      end = wg_tile_at(g, tb, W * (xcd + 1) / NXCD);
     }
   }
   __device__ __forceinline__ Tile next(const GemmArgs& g, const Tables& tb) {
@@ -440,22 +463,43 @@ struct TileIter {
       t.nk = ((K + BK - 1) / BK) * (MODE == DGRAD_GATE_UP ? 2 : 1);
       t.valid = true;
       return t;
+    } else if (!zeros) {
+      const int L = total + j + cpx * i;
+      ++i;
+      if (L >= end) return t;
+      int e = ecache;  // usually the previous tile's expert
+      if (!(unit * tb.nz(e) <= L && L < unit * tb.nz(e + 1))) {
+        int lo = 0, hi = g.E_loc - 1;  // smallest e with unit * nz(e + 1) > L
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (unit * tb.nz(mid + 1) > L) hi = mid; else lo = mid + 1;
+        }
+        e = lo;
+      }
+      ecache = e;
+      t.e = __builtin_amdgcn_readfirstlane(e);
+      const int local = L - unit * tb.nz(e);
+      t.m0 = (local % g.MT) * BM;
+      t.n0 = (local / g.MT) * (DUAL ? BN / 2 : BN);
+      t.seg = tb.off(e);
+      t.ne = tb.off(e + 1) - t.seg;
+      t.nk = (t.ne + BK - 1) / BK;
+      t.valid = true;
+      return t;
     } else {
+      // experts without rows: every one of their tiles, dealt over the grid
       while (true) {
-        const int lt = j + cpx * i;
+        const int G = blockIdx.x + gridDim.x * i;
         ++i;
-        if (lt >= lim) return t;
-        const int k = lt / g.NT, nt = lt % g.NT;
-        const int q = 16 * (k >> 1) + ((k & 1) ? 15 - xcd : xcd);
-        if (q >= gq) continue;
-        t.e = tb.lpt(q / g.MT);
-        t.m0 = (q % g.MT) * BM;
-        t.n0 = nt * (DUAL ? BN / 2 : BN);
-        t.seg = tb.off(t.e);
-        t.ne = tb.off(t.e + 1) - t.seg;
-        t.nk = (t.ne + BK - 1) / BK;
-        if (t.nk == 0 && !zeros) continue;
-        if (t.nk != 0 && zeros) continue;
+        if (G >= g.E_loc * g.MT * g.NT) return t;
+        const int e = G / (g.MT * g.NT), local = G % (g.MT * g.NT);
+        if (tb.off(e + 1) != tb.off(e)) continue;
+        t.e = __builtin_amdgcn_readfirstlane(e);
+        t.m0 = (local % g.MT) * BM;
+        t.n0 = (local / g.MT) * (DUAL ? BN / 2 : BN);
+        t.seg = tb.off(e);
+        t.ne = 0;
+        t.nk = 0;
         t.valid = true;
         return t;
       }
@@ -823,7 +867,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   // tile's last step its A slot (its high halves, when both operands are
   // N-contiguous) holds the epilogue patches; the refill of that slot waits
   // until the epilogue is done.
-  const Tables tb{g.mt_start, g.offsets, g.lpt};
+  const Tables tb{g.mt_start, g.offsets, g.wk_start, g.nz_start};
   const i32x4 nil = make_rsrc(nullptr, 0);
   TileIter<MODE> itc, ita, itb;
   itc.init(g, tb);
@@ -1065,43 +1109,45 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   }
 }
 
-// Per-expert row-tile prefix (mt_start) and experts ordered by row count,
-// descending, ties by index (lpt).  One workgroup, E_loc <= 1024.
+// Per-expert prefixes over experts in index order: row tiles (mt_start), K
+// steps (wk_start) and experts with rows (nz_start).  One workgroup,
+// E_loc <= 1024.
 __global__ __launch_bounds__(1024) void gemm_sched_kernel(const int32_t* __restrict__ offsets,
                                                           int E_loc, int32_t* __restrict__ mt_start,
-                                                          int32_t* __restrict__ lpt) {
-  __shared__ int cnt[1024];
-  __shared__ int wsum[16];
+                                                          int32_t* __restrict__ wk_start,
+                                                          int32_t* __restrict__ nz_start) {
+  __shared__ int wsum[3][16];
   const int e = threadIdx.x;
   const int n = (e < E_loc) ? offsets[e + 1] - offsets[e] : 0;
-  cnt[e] = n;
-  const int mt = (n + BM - 1) / BM;
+  const int v[3] = {(n + BM - 1) / BM, (n + BK - 1) / BK, n > 0 ? 1 : 0};
+  int32_t* const out[3] = {mt_start, wk_start, nz_start};
   const int lane = e & 63, w = e >> 6;
-  int incl = mt;
+  int incl[3] = {v[0], v[1], v[2]};
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += v;
-  }
-  if (lane == 63) wsum[w] = incl;
-  __syncthreads();
-  int base = 0;
-  for (int i = 0; i < w; ++i) base += wsum[i];
-  if (e < E_loc) mt_start[e] = base + incl - mt;
-  if (e == E_loc - 1) mt_start[E_loc] = base + incl;
-  if (e < E_loc) {
-    int rank = 0;
-    for (int o = 0; o < E_loc; ++o) {
-      const int c = cnt[o];
-      rank += (c > n) || (c == n && o < e);
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      const int u = __shfl_up(incl[c], o, 64);
+      if (lane >= o) incl[c] += u;
     }
-    lpt[rank] = e;
+  }
+  if (lane == 63)
+#pragma unroll
+    for (int c = 0; c < 3; ++c) wsum[c][w] = incl[c];
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    int base = 0;
+    for (int q = 0; q < w; ++q) base += wsum[c][q];
+    if (e < E_loc) out[c][e] = base + incl[c] - v[c];
+    if (e == E_loc - 1) out[c][E_loc] = base + incl[c];
   }
 }
 
 struct GemmWs {
   int32_t* mt_start;
-  int32_t* lpt;
+  int32_t* wk_start;
+  int32_t* nz_start;
   uint16_t* act;
   uint16_t* dhg;
   uint16_t* dhu;
@@ -1112,8 +1158,10 @@ GemmWs carve(void* ws, int64_t cap, int E_loc, int f, bool bwd) {
   GemmWs w{};
   w.mt_start = reinterpret_cast<int32_t*>(p);
   p += align_up(sizeof(int32_t) * (E_loc + 1), 256);
-  w.lpt = reinterpret_cast<int32_t*>(p);
-  p += align_up(sizeof(int32_t) * E_loc, 256);
+  w.wk_start = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * (E_loc + 1), 256);
+  w.nz_start = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * (E_loc + 1), 256);
   const size_t act_bytes = align_up(sizeof(uint16_t) * static_cast<size_t>(cap) * f, 256);
   w.act = reinterpret_cast<uint16_t*>(p);
   p += act_bytes;
@@ -1149,7 +1197,7 @@ int64_t pgrid() {
 
 hipError_t sched(const int32_t* offsets, int E_loc, const GemmWs& w, hipStream_t s) {
   prof_begin(K_GEMM_SCHED, s);
-  gemm_sched_kernel<<<1, 1024, 0, s>>>(offsets, E_loc, w.mt_start, w.lpt);
+  gemm_sched_kernel<<<1, 1024, 0, s>>>(offsets, E_loc, w.mt_start, w.wk_start, w.nz_start);
   prof_end(K_GEMM_SCHED, s);
   return hipGetLastError();
 }
@@ -1160,8 +1208,7 @@ size_t gemm_ws_bytes(int64_t cap, int E_loc, int d, int f, unsigned flags) {
   (void)d;
   const bool bwd = flags != 0;
   const size_t act_bytes = align_up(sizeof(uint16_t) * static_cast<size_t>(cap) * f, 256);
-  return align_up(sizeof(int32_t) * (E_loc + 1), 256) + align_up(sizeof(int32_t) * E_loc, 256) +
-         act_bytes * (bwd ? 3 : 1) + 256;
+  return 3 * align_up(sizeof(int32_t) * (E_loc + 1), 256) + act_bytes * (bwd ? 3 : 1) + 256;
 }
 
 hipError_t launch_ffn_fwd(const uint16_t* x_perm, const int32_t* offsets, int E_loc, int64_t cap,
@@ -1172,7 +1219,7 @@ hipError_t launch_ffn_fwd(const uint16_t* x_perm, const int32_t* offsets, int E_
   if (hipError_t e = sched(offsets, E_loc, w, s); e != hipSuccess) return e;
   GemmArgs a{};
   a.x_perm = x_perm; a.wg = wg; a.wu = wu; a.wd = wd;
-  a.offsets = offsets; a.mt_start = w.mt_start; a.lpt = w.lpt;
+  a.offsets = offsets; a.mt_start = w.mt_start; a.wk_start = w.wk_start; a.nz_start = w.nz_start;
   a.hg = hg; a.hu = hu; a.act = w.act; a.act_in = w.act; a.y = y;
   a.E_loc = E_loc; a.d = d; a.f = f;
   a.NT = static_cast<int>(ceil_div(f, BN / 2));
@@ -1193,7 +1240,7 @@ hipError_t launch_ffn_bwd(const uint16_t* dy, const uint16_t* x_perm, const uint
   GemmArgs a{};
   a.x_perm = x_perm; a.wg = wg; a.wu = wu; a.wd = wd;
   a.hg_in = hg; a.hu_in = hu; a.dy = dy;
-  a.offsets = offsets; a.mt_start = w.mt_start; a.lpt = w.lpt;
+  a.offsets = offsets; a.mt_start = w.mt_start; a.wk_start = w.wk_start; a.nz_start = w.nz_start;
   a.dhg = w.dhg; a.dhu = w.dhu; a.act = w.act;
   a.dhg_in = w.dhg; a.dhu_in = w.dhu; a.act_in = w.act;
   a.dx = dx; a.dwg = dwg; a.dwu = dwu; a.dwd = dwd;
