@@ -1090,7 +1090,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
           ring + (A_FIRST ? (NA + ls % NB) : (ls % NA)) * UNIT + w * PATCH_BYTES;
       epilogue(tc, patch);
       zero_acc();
-      wait_vmcnt<0>();  // epilogue stores share the counter with the loads
+      // the patch reads are done once the LDS counter drains; the stores stay
+      // in flight (the next sync's vector-memory wait covers them, in order)
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       __builtin_amdgcn_s_barrier();  // every wave is done with its patch
       __builtin_amdgcn_sched_barrier(0);
       tc = itc.next(g, tb);

@@ -11,84 +11,154 @@
 namespace moe {
 namespace {
 
+typedef int i32x4r __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_byte;
+
+// Compiler-visible wait for every scalar and LDS load of the wave: after it
+// the compiler knows all earlier loads have landed, so the loads issued next
+// (the following batch) stay in flight while the current batch is computed.
+__device__ __forceinline__ void lgkm_drained() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane, global -> LDS (lane i writes LDS [lds + 16 i, +16));
+// completion is tracked by hand with vmcnt.
+__device__ __forceinline__ void w_load_lds16(const i32x4r& rsrc, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
 // Lane = expert (experts lane + 64 b, b < TE); a wave owns TM tokens, a block
-// four waves.  The TM token values are uniform across the wave, so they come
-// in through scalar loads (8 bf16 per load) and feed the FMAs as scalar
-// operands; each lane reads only its own TE router weights from LDS.  W_r
-// is staged in chunks of KC hidden indices, double-buffered: the next chunk
-// is fetched into registers while the current one is consumed.
+// four waves (4 TM tokens).  Each chunk of KC hidden indices moves to
+// LDS with direct-to-LDS loads, NBUF chunks deep: the W_r rows (contiguous in
+// the row-major [d][E] array) and the block's token rows for those indices.
+// Per batch of 8 indices a lane reads its TE weights and, with one broadcast
+// 16-byte read per token, the wave's TM x values; the reads of batch b + 1
+// are issued before batch b is computed (two register sets).
 template <int TM, int TE, int KC>
 __global__ __launch_bounds__(256) void route_logits_kernel(const uint16_t* __restrict__ x,
                                                            const float* __restrict__ w,
                                                            const float* __restrict__ bias,
                                                            int64_t T, int d, int E,
                                                            float* __restrict__ logits) {
-  constexpr int EW = 64 * TE;            // experts covered by one block row
-  constexpr int NW = KC * EW / 256;      // W_r values each thread stages per chunk
-  static_assert(KC % 8 == 0 && (KC * EW) % 256 == 0, "chunk shape");
-  __shared__ __align__(16) float ws[2][KC][EW];
+  constexpr int EW = 64 * TE;                 // experts covered by one block row
+  constexpr int WCH = KC * EW * 4;            // LDS bytes of W_r per chunk (>= KC E 4)
+  constexpr int TB = 4 * TM;                  // tokens per block
+  constexpr int LPWW = WCH / 1024 / 4;        // 1 KiB loads per wave per chunk: W_r
+  constexpr int XPL = 1024 / (KC * 2);        // token rows per 1 KiB x load
+  constexpr int LPWX = (TB + 4 * XPL - 1) / (4 * XPL);  //                      x
+  constexpr int CHUNK = WCH + LPWX * 4 * 1024;  // W_r rows, then the token rows
+  constexpr int NBUF = 4 * CHUNK <= 160 * 1024 ? 4 : 3;
+  static_assert(KC % 8 == 0 && WCH % 4096 == 0 && (KC * 2) <= 1024 && 1024 % (KC * 2) == 0 &&
+                    NBUF * CHUNK <= 160 * 1024,
+                "chunk shape");
+  __shared__ __align__(16) char ws[NBUF * CHUNK];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int64_t tw = static_cast<int64_t>(blockIdx.x) * (4 * TM) + wv * TM;
-  const uint4* xr[TM];
-#pragma unroll
-  for (int a = 0; a < TM; ++a) {
-    const int64_t t = tw + a < T ? tw + a : T - 1;  // tail rows recompute row T-1
-    xr[a] = reinterpret_cast<const uint4*>(x + t * d);
-  }
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * TB;
   float acc[TM][TE];
 #pragma unroll
   for (int a = 0; a < TM; ++a)
 #pragma unroll
     for (int b = 0; b < TE; ++b) acc[a][b] = +0.0f;
 
-  float wr[NW];
-  auto fetch = [&](int j0) {
+  auto rsrc = [](const void* p, int64_t bytes) {
+    const uint64_t addr = reinterpret_cast<uint64_t>(p);
+    i32x4r r;
+    r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(addr & 0xffffffffu));
+    r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((addr >> 32) & 0xffffu));
+    r[2] = static_cast<int>(bytes > 0x7ffffff0 ? 0x7ffffff0 : (bytes < 0 ? 0 : bytes));
+    r[3] = 0x00020000;
+    return r;
+  };
+  // W_r: chunk c = bytes [c KC E 4, +KC E 4); the loads run over WCH bytes
+  // (past the chunk: the next rows or, past the array, zeros), which land
+  // beyond the KC E floats that are read.  x: the block's token rows from t0
+  // (rows past T read as zeros; their logits are never stored).
+  const int64_t wbytes = static_cast<int64_t>(d) * E * 4;
+  const i32x4r rw = rsrc(w, wbytes);
+  const i32x4r rx = rsrc(x + t0 * d, (T - t0) * d * 2);
+  const uint32_t lds0 =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_byte*)(ws)));
+  auto issue_chunk = [&](int c) __attribute__((always_inline)) {
+    const uint32_t dst = lds0 + (c % NBUF) * CHUNK;
+    const int64_t wb = static_cast<int64_t>(c) * KC * E * 4;
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int q = tid + 256 * i, jj = q / EW, ee = q % EW;
-      wr[i] = (j0 + jj < d && ee < E) ? w[static_cast<int64_t>(j0 + jj) * E + ee] : 0.0f;
+    for (int i = 0; i < LPWW; ++i) {
+      const int q = wv * LPWW + i;
+      const int64_t off = wb + q * 1024 + lane * 16;
+      w_load_lds16(rw, off < wbytes ? static_cast<uint32_t>(off) : 0x80000000u, dst + q * 1024);
+    }
+    // x: load q covers token rows XPL q .. XPL q + XPL - 1, KC * 2 bytes each
+#pragma unroll
+    for (int i = 0; i < LPWX; ++i) {
+      const int q = wv * LPWX + i;
+      const int r = q * XPL + lane / (KC / 8);   // token row of this lane
+      const int j = c * KC + (lane % (KC / 8)) * 8;
+      const bool ok = r < TB && j < d;
+      w_load_lds16(rx, ok ? static_cast<uint32_t>((static_cast<int64_t>(r) * d + j) * 2) : 0x80000000u,
+                   dst + WCH + q * 1024);
     }
   };
-  auto stash = [&](int buf) {
+  // one batch = 8 hidden indices: the wave's x words and the lane's weights
+  uint4 xs[2][TM];
+  float wq[2][8][TE];
+  auto issue = [&](int slot, const char* cb, int bl) __attribute__((always_inline)) {
+    const float* cw = reinterpret_cast<const float*>(cb);
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int q = tid + 256 * i;
-      ws[buf][q / EW][q % EW] = wr[i];
-    }
+    for (int a = 0; a < TM; ++a)
+      xs[slot][a] = *reinterpret_cast<const uint4*>(cb + WCH + (wv * TM + a) * (KC * 2) + bl * 16);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int b = 0; b < TE; ++b) wq[slot][u][b] = cw[(bl * 8 + u) * E + lane + 64 * b];
   };
-  const int nch = (d + KC - 1) / KC;
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    const int j0 = c * KC, kc = min(KC, d - j0);  // kc is a multiple of 8
-    if (c + 1 < nch) fetch(j0 + KC);
-    const int buf = c & 1;
-    for (int g = 0; g < kc; g += 8) {
-      uint4 xv[TM];
+  auto compute = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
-      for (int a = 0; a < TM; ++a) xv[a] = xr[a][(j0 + g) >> 3];  // uniform: scalar load
+    for (int u = 0; u < 8; ++u) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        float wl[TE];
+      for (int a = 0; a < TM; ++a) {
+        const uint4 xv = xs[slot][a];
+        const uint32_t pr = u < 2 ? xv.x : u < 4 ? xv.y : u < 6 ? xv.z : xv.w;
+        const float xa = (u & 1) ? bf16_hi(pr) : bf16_lo(pr);
 #pragma unroll
-        for (int b = 0; b < TE; ++b) wl[b] = ws[buf][g + u][lane + 64 * b];
-#pragma unroll
-        for (int a = 0; a < TM; ++a) {
-          const uint32_t pr = u < 2 ? xv[a].x : u < 4 ? xv[a].y : u < 6 ? xv[a].z : xv[a].w;
-          const float xa = (u & 1) ? bf16_hi(pr) : bf16_lo(pr);
-#pragma unroll
-          for (int b = 0; b < TE; ++b) acc[a][b] = __builtin_fmaf(xa, wl[b], acc[a][b]);
-        }
+        for (int b = 0; b < TE; ++b) acc[a][b] = __builtin_fmaf(xa, wq[slot][u][b], acc[a][b]);
       }
     }
-    if (c + 1 < nch) stash(buf ^ 1);
-    __syncthreads();
+  };
+  // lanes of experts past E read weights of other experts: harmless, never stored
+  const int nch = (d + KC - 1) / KC;
+#pragma unroll
+  for (int c = 0; c < NBUF - 1; ++c) issue_chunk(c);
+  for (int c = 0; c < nch; ++c) {
+    wait_vm<(LPWW + LPWX) * (NBUF - 2)>();  // this wave's part of chunk c has landed
+    __syncthreads();                         // everyone's part; chunk c - 1 is consumed
+    issue_chunk(c + NBUF - 1);               // into chunk c - 1's buffer (zeros past the end)
+    const char* cb = ws + (c % NBUF) * CHUNK;
+    const int nbl = min(KC, d - c * KC) / 8;  // batches in this chunk
+    issue(0, cb, 0);
+    for (int bl = 0; bl < nbl; bl += 2) {
+      lgkm_drained();  // batch bl has landed
+      if (bl + 1 < nbl) issue(1, cb, bl + 1);
+      compute(0);
+      if (bl + 1 < nbl) {
+        lgkm_drained();
+        if (bl + 2 < nbl) issue(0, cb, bl + 2);
+        compute(1);
+      }
+    }
   }
+  wait_vm<0>();  // the trailing chunk loads (zeros) are done before the block ends
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
-    const int64_t t = tw + a;
+    const int64_t t = t0 + wv * TM + a;
     if (t >= T) continue;
 #pragma unroll
     for (int b = 0; b < TE; ++b) {
@@ -173,7 +243,8 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
 template <int TM, int TE>
 hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                       int E, float* logits, hipStream_t s) {
-  constexpr int KC = (64 / TE) >= 8 ? (64 / TE) / 8 * 8 : 8;
+  // chunk rows: KC * TE a multiple of 16 (whole 4 KiB per chunk buffer)
+  constexpr int KC = TE == 1 ? 128 : TE == 2 ? 64 : TE == 4 ? 32 : TE <= 8 ? 16 : 8;
   const unsigned grid = static_cast<unsigned>(ceil_div(T, 4 * TM));
   prof_begin(K_ROUTE_LOGITS, s);
   route_logits_kernel<TM, TE, KC><<<grid, 256, 0, s>>>(x, w, bias, T, d, E, logits);
@@ -181,17 +252,18 @@ hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int6
   return hipGetLastError();
 }
 
-// Tokens per wave: the largest of 8, 4, 2, 1 that keeps TM * TE <= 32
-// chains per lane and still launches about 2048 waves (two per SIMD), so
-// that one wave's scalar-load latency is covered by the other's FMAs.
+// Tokens per wave: about one block per CU (T / 1024 tokens per wave,
+// rounded down to 8, 4, 2 or 1), so that every block reads W_r once for as
+// many tokens as the chip's share allows, with at most 64 accumulators per
+// lane (TM * TE <= 64).
 template <int TE>
 hipError_t pick_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                        int E, float* logits, hipStream_t s) {
-  if constexpr (TE <= 4)
-    if (T >= 8 * 2048) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
-  if constexpr (TE <= 8)
-    if (T >= 4 * 2048) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
-  if (T >= 2 * 2048) return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
+  if constexpr (8 * TE <= 64)
+    if (T >= 8 * 1024) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
+  if constexpr (4 * TE <= 64)
+    if (T >= 4 * 1024) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
+  if (T >= 2 * 1024) return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
   return run_logits<1, TE>(x, w, bias, T, d, E, logits, s);
 }
 
