@@ -158,6 +158,50 @@ def stored_traffic(workload: str, kernel: str):
     return found["read_bytes"] + found["write_bytes"]
 
 
+def chunked_forward(layer, steps: int):
+    """Memory-efficient forward (token chunks on two streams) against the
+    unchunked forward: time per forward and transient buffer bytes."""
+    import ctypes
+    m, wl, inp = layer.moe, layer.wl, layer.inp
+    dev = inp["x"].device
+    side = torch.cuda.Stream(device=dev)
+    y = torch.empty((wl.T, wl.d), dtype=torch.bfloat16, device=dev)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / steps
+
+    def unchunked():
+        pm = layer._permute_into()
+        m.moe_grouped_swiglu_fwd(pm["x_perm"], pm["expert_offsets"], inp["w_gate"], inp["w_up"],
+                                 inp["w_down"], cap=wl.cap, h_gate=layer.hg, h_up=layer.hu,
+                                 y_perm=layer.yp)
+        m.moe_combine(layer.yp, pm["dst"], layer.gate, out=y)
+
+    cap, d, f = wl.cap, wl.d, wl.f
+    full_bytes = cap * (2 * d + 3 * f) * 2  # x_perm, y_perm, h_gate, h_up, act
+    out = {"unchunked": {"ms": round(timed(unchunked), 4), "transient_bytes": full_bytes}}
+    for parts in (2, 4, 8):
+        chunk = -(-wl.T // parts)
+        n = ctypes.c_size_t()
+        m._check(m.lib.moe_ffn_fwd_chunked_workspace_bytes(chunk, wl.E, wl.k, wl.E_loc, d, f,
+                                                           ctypes.byref(n)),
+                 "moe_ffn_fwd_chunked_workspace_bytes")
+        ms = timed(lambda: m.moe_ffn_fwd_chunked(inp["x"], layer.idx, layer.gate, wl.E,
+                                                 inp["w_gate"], inp["w_up"], inp["w_down"], chunk,
+                                                 wl.expert_begin, wl.E_loc, out=y, stream2=side))
+        out[f"chunks_{parts}"] = {"chunk_tokens": chunk, "ms": round(ms, 4),
+                                  "transient_bytes": int(n.value)}
+    return out
+
+
 def cpu_baseline(wl, inp, budget_s: float):
     """The oracle (as is) on the first T_s tokens of the same workload."""
     import oracle
@@ -273,6 +317,9 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    memfwd = chunked_forward(layer, args.steps)
+    log(f"[bench] memory-efficient forward: {memfwd}")
+
     cpu = None
     if args.cpu_budget > 0:
         log("[bench] cpu baseline ...")
@@ -291,6 +338,7 @@ def main():
         else round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
         "with_router_backward": {"ms_per_step": round(ms_rb, 4),
                                  "value": round(wl.T / (ms_rb * 1e-3), 1), "unit": "tokens/s"},
+        "memory_efficient_forward": memfwd,
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,

@@ -211,6 +211,38 @@ int moe_combine_bwd(const moe_bf16* dout, const moe_bf16* y_perm, const int32_t*
                     const float* topk_gate, int64_t T, int d, int k, moe_bf16* dy_perm,
                     float* dgate, void* stream);
 
+/* ---------------------------------------------- memory-efficient forward
+ * The expert layer's forward over chunks of `chunk` tokens (Sec. 3.3, the
+ * memory-efficient variant: overlap the movement of routed rows with the
+ * expert computation so that only a small fraction of the routed inputs,
+ * dispatch buffers and expert intermediates is resident at once; eq. (peaks)
+ * names that O(N k H + N_r I) transient).  For tokens [c*chunk, (c+1)*chunk)
+ * it runs moe_permute, moe_grouped_swiglu_fwd and moe_combine (weighted by
+ * topk_gate) into y, alternating chunks between `stream` and `stream2` with
+ * two sets of transient buffers inside the workspace: the transient peak is
+ * that of two chunks instead of all T tokens, and one chunk's permutation
+ * and combine overlap the other chunk's grouped GEMMs.  Every row of y
+ * depends on its own token only, so y is bit-identical to the unchunked
+ * forward.  No backward state is kept (x_perm, h_gate, h_up are transient).
+ *
+ * x [T][d] bf16; topk_idx, topk_gate [T][k]; weights as for
+ * moe_grouped_swiglu_fwd; y [T][d] bf16 (tokens with no local expert get 0).
+ * workspace: moe_ffn_fwd_chunked_workspace_bytes(chunk, ...) bytes (it does
+ * not depend on T).  `stream` is the caller's stream: the inputs must be
+ * ready on it and the call's work is complete on it.  `stream2` may equal
+ * `stream` (no overlap) or be another stream of the same device (made to
+ * wait for `stream` first).  The library keeps one HIP event per device for
+ * the two cross-stream waits.  The optional kernel profiler attributes the
+ * two streams' interleaved kernels only approximately.
+ */
+int moe_ffn_fwd_chunked_workspace_bytes(int64_t chunk, int E, int k, int num_local, int d, int f,
+                                        size_t* bytes);
+int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, const float* topk_gate,
+                        int64_t T, int d, int E, int k, int expert_begin, int num_local, int f,
+                        const moe_bf16* w_gate, const moe_bf16* w_up, const moe_bf16* w_down,
+                        int64_t chunk, moe_bf16* y, void* workspace, size_t workspace_bytes,
+                        void* stream, void* stream2);
+
 /* ------------------------------------------------------------- profiling
  * Optional per-kernel timing with HIP events recorded on the launch stream
  * around every kernel the library enqueues (for measurement only; off by

@@ -105,6 +105,12 @@ hipError_t launch_route_bwd(const uint16_t* x, const float* w, const float* logi
                             int64_t T, int d, int E, int k, int renorm, float* dw, float* dbias,
                             uint16_t* dx, int dx_accumulate, float* dlogits, void* ws,
                             hipStream_t s);
+size_t ffn_fwd_chunked_ws_bytes(int64_t chunk, int E, int k, int E_loc, int d, int f);
+hipError_t launch_ffn_fwd_chunked(const uint16_t* x, const int32_t* idx, const float* gate,
+                                  int64_t T, int d, int E, int k, int e_begin, int E_loc, int f,
+                                  const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
+                                  int64_t chunk, uint16_t* y, void* ws, hipStream_t s0,
+                                  hipStream_t s1);
 size_t permute_ws_bytes(int64_t T, int E, int k, int E_loc);
 hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int d, int E, int k,
                           int e_begin, int E_loc, int32_t* offsets, int32_t* counts_global,

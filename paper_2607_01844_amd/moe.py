@@ -29,6 +29,7 @@ C_SYMBOLS = (
     "moe_permute_workspace_bytes", "moe_permute",
     "moe_grouped_swiglu_workspace_bytes", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
     "moe_combine", "moe_combine_bwd",
+    "moe_ffn_fwd_chunked_workspace_bytes", "moe_ffn_fwd_chunked",
     "moe_profile_enable", "moe_profile_reset", "moe_profile_num_kernels",
     "moe_profile_kernel_name", "moe_profile_query",
 )
@@ -62,6 +63,8 @@ def _load():
                                     P], I),
         "moe_combine": ([P, P, P, I64, I, I, P, P], I),
         "moe_combine_bwd": ([P, P, P, P, I64, I, I, P, P, P], I),
+        "moe_ffn_fwd_chunked_workspace_bytes": ([I64, I, I, I, I, I, PSZ], I),
+        "moe_ffn_fwd_chunked": ([P, P, P, I64, I, I, I, I, I, I, P, P, P, I64, P, P, SZ, P, P], I),
         "moe_profile_enable": ([I], I),
         "moe_profile_reset": ([], I),
         "moe_profile_num_kernels": ([], I),
@@ -309,6 +312,33 @@ def moe_combine_bwd(dout, y_perm, dst, topk_gate, dy_perm=None, dgate=None, with
     _check(lib.moe_combine_bwd(_ptr(dout), _ptr(y_perm), _ptr(dst), _ptr(topk_gate), T, d, k,
                                _ptr(dy_perm), _ptr(dgate), _stream()), "moe_combine_bwd")
     return dy_perm, dgate
+
+
+def moe_ffn_fwd_chunked(x, topk_idx, topk_gate, E, w_gate, w_up, w_down, chunk, expert_begin=0,
+                        num_local=None, out=None, stream2=None):
+    """Memory-efficient forward over token chunks on the current stream and
+    `stream2` (a torch.cuda.Stream or None = the current stream).  Returns y."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(topk_idx, torch.int32, "topk_idx", 2)
+    _need(topk_gate, torch.float32, "topk_gate", 2)
+    for n, w in (("w_gate", w_gate), ("w_up", w_up), ("w_down", w_down)):
+        _need(w, torch.bfloat16, n, 3)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    num_local = w_gate.shape[0] if num_local is None else num_local
+    f = w_gate.shape[2]
+    if out is None:
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=x.device)
+    n = ctypes.c_size_t()
+    _check(lib.moe_ffn_fwd_chunked_workspace_bytes(chunk, E, k, num_local, d, f, ctypes.byref(n)),
+           "moe_ffn_fwd_chunked_workspace_bytes")
+    ws = workspace(n.value, x.device, "ffn_fwd_chunked")
+    s2 = _stream() if stream2 is None else ctypes.c_void_p(stream2.cuda_stream)
+    _check(lib.moe_ffn_fwd_chunked(_ptr(x), _ptr(topk_idx), _ptr(topk_gate), T, d, E, k,
+                                   expert_begin, num_local, f, _ptr(w_gate), _ptr(w_up),
+                                   _ptr(w_down), chunk, _ptr(out), _ptr(ws), ws.numel(), _stream(),
+                                   s2), "moe_ffn_fwd_chunked")
+    return out
 
 
 # ------------------------------------------------------------- profiling

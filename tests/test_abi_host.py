@@ -100,6 +100,18 @@ Z = None
                                                          P, Z, P, P, 2, P, 1 << 20, Z)),
     ("combine k", lambda L: L.moe_combine(P, P, P, 10, 64, 0, P, Z)),
     ("combine_bwd d", lambda L: L.moe_combine_bwd(P, P, P, P, 10, 4, 2, P, P, Z)),
+    ("route_bwd renorm", lambda L: L.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 3, P, Z, Z, 1,
+                                                   Z, P, 1 << 20, Z)),
+    ("route_bwd null dw", lambda L: L.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, Z, Z, Z, 1,
+                                                    Z, P, 1 << 20, Z)),
+    ("route_bwd accumulate", lambda L: L.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, P, Z, P,
+                                                       2, Z, P, 1 << 20, Z)),
+    ("chunked chunk 0", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 32, P, P, P,
+                                                        0, P, P, 1 << 20, Z, Z)),
+    ("chunked range", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 4, 8, 32, P, P, P, 4,
+                                                      P, P, 1 << 20, Z, Z)),
+    ("chunked f % 8", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 30, P, P, P, 4,
+                                                      P, P, 1 << 20, Z, Z)),
 ])
 def test_invalid_arguments_rejected_on_host(lib, case):
     name, call = case
@@ -112,3 +124,19 @@ def test_workspace_too_small_rejected(lib):
     assert lib.moe_permute(P, P, 10, 64, 8, 2, 0, 8, P, Z, P, P, P, P, 16, Z) == -3
     assert lib.moe_grouped_swiglu_fwd(P, P, 4, 100, 64, 32, P, P, P, P, P, P, P, 16, Z) == -3
     assert lib.moe_route(P, P, Z, 10, 64, 8, 2, 0, P, P, Z, P, 16, Z) == -3
+    assert lib.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, P, Z, Z, 1, Z, P, 16, Z) == -3
+    assert lib.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 32, P, P, P, 4, P, P, 16, Z,
+                                   Z) == -3
+
+
+def test_chunked_workspace_depends_on_chunk_only(lib):
+    """The memory-efficient forward's workspace holds two chunks' transient
+    buffers: linear in the chunk, independent of T."""
+    n1, n2 = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.moe_ffn_fwd_chunked_workspace_bytes(512, 64, 6, 64, 2048, 1408, ctypes.byref(n1)) == 0
+    assert lib.moe_ffn_fwd_chunked_workspace_bytes(1024, 64, 6, 64, 2048, 1408,
+                                                   ctypes.byref(n2)) == 0
+    rows = 512 * 6  # routed rows of one 512-token chunk
+    per_set = rows * (2 * 2048 + 3 * 1408) * 2  # x_perm, y_perm, h_gate, h_up, act
+    assert n1.value >= 2 * per_set
+    assert 1.9 < n2.value / n1.value < 2.1
