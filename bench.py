@@ -127,33 +127,32 @@ def kernel_table(wl, M, T_touched, prof, steps):
     return rows, flops, bytes_
 
 
-TRAFFIC_SOURCES = ("paper_2607_01844_amd/csrc/gemm.hip", "paper_2607_01844_amd/csrc/common.h")
+TRAFFIC_SOURCE = "gemm.hip"  # the object whose machine code the stored counters belong to
 
 
 def stored_traffic(workload: str, kernel: str):
     """HBM-side bytes per launch of `kernel` from the committed counter summary
     (FETCH_SIZE / WRITE_SIZE passes scaled by a plain copy of known size), or
-    None when there is no summary for this workload or the kernel sources have
-    changed since it was taken."""
-    import hashlib
+    None when there is no summary for this workload or the grouped GEMMs'
+    machine code differs from the code the summary was measured on."""
+    import json
     path = os.path.join(ROOT, "profiles", f"moe_layer_{workload}_hbm_traffic.txt")
-    if not os.path.exists(path):
+    built = os.path.join(ROOT, "paper_2607_01844_amd", "libmoe.device_text.json")
+    if not os.path.exists(path) or not os.path.exists(built):
         return None
-    h = hashlib.sha256()
-    for p in TRAFFIC_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as fh:
-            h.update(fh.read())
+    with open(built) as fh:
+        now = json.load(fh).get(TRAFFIC_SOURCE)
     src, found = None, None
     with open(path) as fh:
         for line in fh:
             f = line.split()
             if not f or f[0].startswith("#"):
                 continue
-            if f[0] == "source_sha256":
-                src = f[1]
+            if f[0] == "device_text_sha256" and f[1] == TRAFFIC_SOURCE:
+                src = f[2]
             elif f[0] == "kernel" and f[1] == kernel:
                 found = {kv.split("=")[0]: int(kv.split("=")[1]) for kv in f[2:]}
-    if src != h.hexdigest() or found is None:
+    if now is None or src != now or found is None:
         return None
     return found["read_bytes"] + found["write_bytes"]
 
@@ -202,6 +201,60 @@ def chunked_forward(layer, steps: int):
     return out
 
 
+def vocab_loss(steps: int, warmup: int):
+    """Blockwise vocabulary loss on its own workload (Sec. 3.4): forward,
+    backward and both, with the dense-equivalent FLOP rate (2NHV forward,
+    6NHV backward: the logits are recomputed there) and the resident bytes
+    against those of the dense N x V logits."""
+    import ctypes
+    from paper_2607_01844_amd import moe as m
+    vw = W.VOCAB_WORKLOADS["vocab_mid"]
+    inp = W.make_vocab_inputs(vw, seed=0, device="cuda")
+    x, w, t, dl = inp["x"], inp["w_voc"], inp["target"], inp["dloss"]
+    loss = torch.empty((vw.N,), dtype=torch.float32, device="cuda")
+    lse = torch.empty_like(loss)
+    dx = torch.empty_like(x)
+    dw = torch.empty_like(w)
+    fwd = lambda: m.moe_vocab_loss_fwd(x, w, t, vw.vblock, loss=loss, lse=lse)  # noqa: E731
+    bwd = lambda: m.moe_vocab_loss_bwd(x, w, t, lse, dl, vw.vblock, dx=dx, dw_voc=dw)  # noqa
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / steps
+
+    f_ms, b_ms = timed(fwd), timed(bwd)
+    both = timed(lambda: (fwd(), bwd()))
+    nhv = vw.N * vw.H * vw.V
+    tf = 8.0 * nhv / (both * 1e-3) / 1e12
+    n = ctypes.c_size_t()
+    m._check(m.lib.moe_vocab_loss_workspace_bytes(vw.N, vw.H, vw.V, vw.vblock, ctypes.byref(n)),
+             "moe_vocab_loss_workspace_bytes")
+    m.profile_reset()
+    m.profile_enable(True)
+    for _ in range(steps):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    m.profile_enable(False)
+    prof = m.profile_query()
+    m.profile_reset()
+    ks = {k: {"us_per_step": round(v[0] / steps * 1e3, 1), "launches_per_step": v[1] // steps}
+          for k, v in prof.items() if k.startswith("vocab")}
+    return {"workload": vw.describe(), "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
+            "fwd_bwd_ms": round(both, 4), "tokens_per_s": round(vw.N / (both * 1e-3), 1),
+            "dense_equiv_tflops": round(tf, 1), "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+            "workspace_bytes": int(n.value), "dense_logits_bytes": 4 * vw.N * vw.V,
+            "kernels": ks}
+
+
 def cpu_baseline(wl, inp, budget_s: float):
     """The oracle (as is) on the first T_s tokens of the same workload."""
     import oracle
@@ -237,6 +290,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-vocab", action="store_true", help="skip the vocabulary-loss leg")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
@@ -320,6 +374,13 @@ def main():
     memfwd = chunked_forward(layer, args.steps)
     log(f"[bench] memory-efficient forward: {memfwd}")
 
+    voc = None
+    if not args.no_vocab:
+        del layer
+        torch.cuda.empty_cache()
+        voc = vocab_loss(args.steps, args.warmup)
+        log(f"[bench] vocabulary loss: {voc}")
+
     cpu = None
     if args.cpu_budget > 0:
         log("[bench] cpu baseline ...")
@@ -339,6 +400,7 @@ def main():
         "with_router_backward": {"ms_per_step": round(ms_rb, 4),
                                  "value": round(wl.T / (ms_rb * 1e-3), 1), "unit": "tokens/s"},
         "memory_efficient_forward": memfwd,
+        "vocab_loss": voc,
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,

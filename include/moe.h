@@ -15,7 +15,8 @@
  *  - bf16 values are raw IEEE bfloat16 bit patterns (moe_bf16); fp32->bf16 is
  *    round-to-nearest-even.  All arrays are dense and row-major.
  *  - Every pointer is DEVICE memory owned by the caller; the library
- *    allocates nothing and keeps no reference after the call returns.
+ *    allocates nothing (save the vocabulary loss's rocBLAS handle) and
+ *    keeps no reference after the call returns.
  *    Required pointers must be non-NULL and 16-byte aligned.
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *    Calls only enqueue work and return; no call synchronises the device.
@@ -242,6 +243,40 @@ int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, const float*
                         const moe_bf16* w_gate, const moe_bf16* w_up, const moe_bf16* w_down,
                         int64_t chunk, moe_bf16* y, void* workspace, size_t workspace_bytes,
                         void* stream, void* stream2);
+
+/* ------------------------------------------------------- vocabulary loss
+ * Blockwise online loss of the vocabulary projection (Sec. 3.4, eq.
+ * (voc-fwd-loss): Y = X W_voc, loss_n = Y[n][t_n] - log sum_v exp Y[n][v]),
+ * on one device with the vocabulary walked in blocks of `vblock` columns
+ * instead of split over ranks: only an N x vblock slice of the logits is
+ * resident at any instant, never the N x V tensor, and the loss and its
+ * gradients are those of the dense projection up to rounding.
+ *
+ * x [N][H] bf16; w_voc [H][V] bf16; target [N] int32 in [0, V) (a target
+ * outside [0, V) is undefined behaviour).  Logits are fp32 sums of bf16
+ * products.  moe_vocab_loss_fwd writes loss [N] fp32 (the log-likelihood
+ * of the target, <= 0) and lse [N] fp32 (log sum_v exp Y[n][v]), which the
+ * backward takes back.  moe_vocab_loss_bwd, given dloss [N] fp32 =
+ * dL/dloss, recomputes each block of logits and writes
+ *   dx [N][H]  bf16 = sum_v G[n][v] W_voc[:, v]  (fp32 across blocks)
+ *   dw_voc [H][V] bf16 = X^T G  (every column written; zeros when N = 0)
+ * with G[n][v] = dloss_n ([v == t_n] - exp(Y[n][v] - lse_n)) rounded to
+ * bf16 before the two products.  Limits: 0 <= N < 2^31, 1 <= V < 2^31, H a
+ * multiple of 8, vblock a positive multiple of 8, N * vblock < 2^40.
+ * workspace: moe_vocab_loss_workspace_bytes() bytes (serves both calls;
+ * about 6 N vblock + 4 N H bytes + 32 MiB).  The three products per block
+ * are rocBLAS GEMMs: the first call on a device creates that device's
+ * rocBLAS handle (the one allocation the library makes; it is kept until
+ * the process ends), and calls on one device serialise on its host lock.
+ */
+int moe_vocab_loss_workspace_bytes(int64_t N, int H, int64_t V, int64_t vblock, size_t* bytes);
+int moe_vocab_loss_fwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* target, int64_t N,
+                       int H, int64_t V, int64_t vblock, float* loss, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream);
+int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* target,
+                       const float* lse, const float* dloss, int64_t N, int H, int64_t V,
+                       int64_t vblock, moe_bf16* dx, moe_bf16* dw_voc, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------- profiling
  * Optional per-kernel timing with HIP events recorded on the launch stream

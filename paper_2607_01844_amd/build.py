@@ -5,16 +5,23 @@
 from __future__ import annotations
 
 import concurrent.futures as cf
+import hashlib
+import json
 import os
 import subprocess
 import sys
+import tempfile
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmoe.so")
-SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "chunked.hip"]
+# sha256 of each object's gfx950 machine code (.text of its device code
+# object), written beside the library at every build: a stored measurement
+# names the code it was taken on, and stays valid while that code is unchanged
+DEVICE_TEXT = os.path.join(PKG, "libmoe.device_text.json")
+SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "chunked.hip", "vocab.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -40,17 +47,47 @@ def _compile(src: str) -> str:
     return obj
 
 
+LLVM = "/opt/rocm/llvm/bin"
+
+
+def device_text_sha256(obj: str) -> str:
+    """sha256 of the .text section of the gfx950 code object embedded in a
+    hipcc object file (comments and host-only edits leave it unchanged), or
+    None for an object without device code."""
+    sections = subprocess.run([f"{LLVM}/llvm-readelf", "-S", obj], check=True,
+                              capture_output=True, text=True).stdout
+    if ".hip_fatbin" not in sections:
+        return None
+    with tempfile.TemporaryDirectory() as tmp:
+        fat, co, text = (os.path.join(tmp, n) for n in ("fat.bin", "dev.co", "text.bin"))
+        subprocess.run([f"{LLVM}/llvm-objcopy", "-O", "binary", "--only-section=.hip_fatbin", obj,
+                        fat], check=True, capture_output=True)
+        subprocess.run([f"{LLVM}/clang-offload-bundler", "--unbundle", "--type=o",
+                        f"--input={fat}", f"--targets=hipv4-amdgcn-amd-amdhsa--{ARCH}",
+                        f"--output={co}"], check=True, capture_output=True)
+        subprocess.run([f"{LLVM}/llvm-objcopy", "-O", "binary", "--only-section=.text", co, text],
+                       check=True, capture_output=True)
+        with open(text, "rb") as fh:
+            return hashlib.sha256(fh.read()).hexdigest()
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source for gfx950 and link libmoe.so (always rebuilds)."""
     os.makedirs(OBJ, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    # rocBLAS runs the vocabulary projection's plain dense products
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-L/opt/rocm/lib",
+           "-lrocblas", "-Wl,-rpath,/opt/rocm/lib", "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     os.replace(tmp, LIB)
+    hashes = {src: device_text_sha256(obj) for src, obj in zip(SOURCES, objs)}
+    with open(DEVICE_TEXT + ".tmp", "w") as fh:
+        json.dump(hashes, fh, indent=1, sort_keys=True)
+    os.replace(DEVICE_TEXT + ".tmp", DEVICE_TEXT)
     if verbose:
         print("built", LIB)
     return LIB

@@ -87,7 +87,7 @@ const char* const kNames[moe::K_NUM] = {
     "permute_rank", "permute_gather",  "gemm_sched",         "gemm_fwd_gate_up",
     "gemm_fwd_down", "gemm_dgrad_down", "gemm_dgrad_gate_up", "gemm_wgrad_gate_up",
     "gemm_wgrad_down", "combine",       "combine_bwd",        "route_dlogits",
-    "route_dw",     "route_dx"};
+    "route_dw",     "route_dx",        "vocab_lse",          "vocab_grad"};
 
 }  // namespace
 
@@ -387,6 +387,60 @@ MOE_API int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, cons
                                                 num_local, f, w_gate, w_up, w_down, chunk, y,
                                                 workspace, static_cast<hipStream_t>(stream),
                                                 static_cast<hipStream_t>(stream2)),
+                    fn);
+}
+
+// ------------------------------------------------------ vocabulary loss
+static int check_vocab(const char* fn, int64_t N, int H, int64_t V, int64_t vblock) {
+  CHECK(N >= 0 && N < (int64_t{1} << 31), "N out of [0, 2^31)");
+  if (int r = check_dim(fn, H, "H")) return r;
+  CHECK(V >= 1 && V < (int64_t{1} << 31), "V out of [1, 2^31)");
+  CHECK(vblock >= 8 && (vblock % 8) == 0, "vblock must be a positive multiple of 8");
+  CHECK(N * vblock < (int64_t{1} << 40), "N*vblock too large");
+  return MOE_OK;
+}
+
+MOE_API int moe_vocab_loss_workspace_bytes(int64_t N, int H, int64_t V, int64_t vblock,
+                                           size_t* bytes) {
+  const char* fn = "moe_vocab_loss_workspace_bytes";
+  CHECK(bytes != nullptr, "bytes is NULL");
+  if (int r = check_vocab(fn, N, H, V, vblock)) return r;
+  *bytes = std::max(moe::vocab_fwd_ws_bytes(N, vblock), moe::vocab_bwd_ws_bytes(N, H, vblock));
+  return MOE_OK;
+}
+
+MOE_API int moe_vocab_loss_fwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* target,
+                               int64_t N, int H, int64_t V, int64_t vblock, float* loss,
+                               float* lse, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  const char* fn = "moe_vocab_loss_fwd";
+  if (int r = check_vocab(fn, N, H, V, vblock)) return r;
+  if (N > 0) {
+    REQ(x); REQ(w_voc); REQ(target); REQ(loss); REQ(lse);
+    if (workspace == nullptr || workspace_bytes < moe::vocab_fwd_ws_bytes(N, vblock))
+      return fail(MOE_ERR_WORKSPACE, fn, "workspace smaller than moe_vocab_loss_workspace_bytes()");
+    OPT(workspace);
+  }
+  return hip_status(moe::launch_vocab_fwd(x, w_voc, target, N, H, V, vblock, loss, lse,
+                                          workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+MOE_API int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* target,
+                               const float* lse, const float* dloss, int64_t N, int H, int64_t V,
+                               int64_t vblock, moe_bf16* dx, moe_bf16* dw_voc, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  const char* fn = "moe_vocab_loss_bwd";
+  if (int r = check_vocab(fn, N, H, V, vblock)) return r;
+  REQ(dw_voc);
+  if (N > 0) {
+    REQ(x); REQ(w_voc); REQ(target); REQ(lse); REQ(dloss); REQ(dx);
+    if (workspace == nullptr || workspace_bytes < moe::vocab_bwd_ws_bytes(N, H, vblock))
+      return fail(MOE_ERR_WORKSPACE, fn, "workspace smaller than moe_vocab_loss_workspace_bytes()");
+    OPT(workspace);
+  }
+  return hip_status(moe::launch_vocab_bwd(x, w_voc, target, lse, dloss, N, H, V, vblock, dx,
+                                          dw_voc, workspace, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

@@ -83,6 +83,8 @@ enum KernelId {
   K_ROUTE_DLOGITS,
   K_ROUTE_DW,
   K_ROUTE_DX,
+  K_VOC_LSE,
+  K_VOC_GRAD,
   K_NUM
 };
 
@@ -105,6 +107,14 @@ hipError_t launch_route_bwd(const uint16_t* x, const float* w, const float* logi
                             int64_t T, int d, int E, int k, int renorm, float* dw, float* dbias,
                             uint16_t* dx, int dx_accumulate, float* dlogits, void* ws,
                             hipStream_t s);
+size_t vocab_fwd_ws_bytes(int64_t N, int64_t vblock);
+size_t vocab_bwd_ws_bytes(int64_t N, int H, int64_t vblock);
+hipError_t launch_vocab_fwd(const uint16_t* x, const uint16_t* w, const int32_t* target,
+                            int64_t N, int H, int64_t V, int64_t vblock, float* loss, float* lse,
+                            void* ws, hipStream_t s);
+hipError_t launch_vocab_bwd(const uint16_t* x, const uint16_t* w, const int32_t* target,
+                            const float* lse, const float* dloss, int64_t N, int H, int64_t V,
+                            int64_t vblock, uint16_t* dx, uint16_t* dw, void* ws, hipStream_t s);
 size_t ffn_fwd_chunked_ws_bytes(int64_t chunk, int E, int k, int E_loc, int d, int f);
 hipError_t launch_ffn_fwd_chunked(const uint16_t* x, const int32_t* idx, const float* gate,
                                   int64_t T, int d, int E, int k, int e_begin, int E_loc, int f,

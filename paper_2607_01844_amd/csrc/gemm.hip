@@ -2,18 +2,22 @@
 //
 // Every GEMM of the expert FFN (forward gate/up and down, data gradients,
 // weight gradients) is one instance of a single macro-tile kernel:
-//   * 256 threads = 4 waves in a 2 x 2 grid; the block computes a 256 x 256
-//     tile of C^T (rows = output columns n, cols = output rows m) with
-//     v_mfma_f32_32x32x16_bf16, so each lane ends up holding four consecutive
-//     output columns and stores 8 bytes at a time.
+//   * 512 threads = 8 waves (two per SIMD) in a 2 x 4 grid; the block
+//     computes a 256 x 256 tile of C^T (rows = output columns n, cols =
+//     output rows m) with v_mfma_f32_32x32x16_bf16, each wave 128 rows x 64
+//     columns, so each lane ends up holding four consecutive output columns
+//     and stores 8 bytes at a time.
 //   * Operands move global -> LDS with buffer_load_dwordx4 ... lds (no
 //     register staging).  The buffer descriptor's range check turns every
 //     tail (rows past an expert's segment, k past K, columns past N) into
 //     zeros, so there is no padding and no per-element branching.
-//   * K steps of 64 in a ring of 2 LDS stages (128 KiB of the 160 KiB):
-//     loads run one step ahead of the MFMAs; one barrier per step.  A step
-//     of 64 k makes every row of a K-contiguous tile one full 128-byte line,
-//     which the memory path moves at twice the rate of 64-byte halves.
+//   * K steps of 64 through a ring of five 32 KiB LDS slots (all 160 KiB):
+//     two for the operand the tile streams fastest and three for the other,
+//     so loads run up to three steps ahead of the MFMAs, spread evenly over
+//     the sub-steps between barriers; one barrier per step, and the stream
+//     of K steps continues across tile boundaries.  A step of 64 k makes
+//     every row of a K-contiguous tile one full 128-byte line, which the
+//     memory path moves at twice the rate of 64-byte halves.
 //   * Operands stored K-contiguous (activations in the forward pass and the
 //     data gradients, weights in the data gradients) sit in LDS as
 //     [256 rows][64 k] and feed the MFMA with ds_read_b128.  Operands stored
@@ -135,38 +139,6 @@ __device__ __forceinline__ void load_2x4_wait(const i32x4& ra, const i32x4& rb, 
       : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(ra), "s"(rb)
       : "memory");
 }
-// Sixteen 16-byte loads into registers (eight from each of two buffers, same
-// offsets) that complete inside the statement: the compiler never sees them
-// in flight, so its own counter bookkeeping stays exact around the K loop.
-// Waits for every vector-memory operation of the wave.
-__device__ __forceinline__ void load_2x8_wait(const i32x4& ra, const i32x4& rb, const uint32_t (&off)[8],
-                                              u32x4a (&a)[8], u32x4a (&b)[8]) {
-  asm volatile(
-      "buffer_load_dwordx4 %0, %16, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %1, %17, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %2, %18, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %3, %19, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %4, %20, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %5, %21, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %6, %22, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %7, %23, %24, 0 offen\n\t"
-      "buffer_load_dwordx4 %8, %16, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %9, %17, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %10, %18, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %11, %19, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %12, %20, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %13, %21, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %14, %22, %25, 0 offen\n\t"
-      "buffer_load_dwordx4 %15, %23, %25, 0 offen\n\t"
-      "s_waitcnt vmcnt(0)"
-      : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3]), "=&v"(a[4]), "=&v"(a[5]), "=&v"(a[6]),
-        "=&v"(a[7]), "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3]), "=&v"(b[4]), "=&v"(b[5]),
-        "=&v"(b[6]), "=&v"(b[7])
-      : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]), "v"(off[5]), "v"(off[6]),
-        "v"(off[7]), "s"(ra), "s"(rb)
-      : "memory");
-}
-
 // ------------------------------------------------------- K-major operand
 // Tile rows r (m or n) with k contiguous: element (r, k) of source s at
 // byte r*ld + 2k from its base.  Dual-K: steps [0, nk0) read source 0,
@@ -350,10 +322,6 @@ struct GemmArgs {
   int NT;  // column tiles per row tile
   int MT;  // row tiles per expert (weight-gradient modes)
 };
-
-__device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
 
 __device__ __forceinline__ uint2 pack4(float a, float b, float c, float d) {
   return make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));

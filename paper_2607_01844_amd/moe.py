@@ -30,6 +30,7 @@ C_SYMBOLS = (
     "moe_grouped_swiglu_workspace_bytes", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
     "moe_combine", "moe_combine_bwd",
     "moe_ffn_fwd_chunked_workspace_bytes", "moe_ffn_fwd_chunked",
+    "moe_vocab_loss_workspace_bytes", "moe_vocab_loss_fwd", "moe_vocab_loss_bwd",
     "moe_profile_enable", "moe_profile_reset", "moe_profile_num_kernels",
     "moe_profile_kernel_name", "moe_profile_query",
 )
@@ -65,6 +66,9 @@ def _load():
         "moe_combine_bwd": ([P, P, P, P, I64, I, I, P, P, P], I),
         "moe_ffn_fwd_chunked_workspace_bytes": ([I64, I, I, I, I, I, PSZ], I),
         "moe_ffn_fwd_chunked": ([P, P, P, I64, I, I, I, I, I, I, P, P, P, I64, P, P, SZ, P, P], I),
+        "moe_vocab_loss_workspace_bytes": ([I64, I, I64, I64, PSZ], I),
+        "moe_vocab_loss_fwd": ([P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
+        "moe_vocab_loss_bwd": ([P, P, P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
         "moe_profile_enable": ([I], I),
         "moe_profile_reset": ([], I),
         "moe_profile_num_kernels": ([], I),
@@ -339,6 +343,54 @@ def moe_ffn_fwd_chunked(x, topk_idx, topk_gate, E, w_gate, w_up, w_down, chunk, 
                                    _ptr(w_down), chunk, _ptr(out), _ptr(ws), ws.numel(), _stream(),
                                    s2), "moe_ffn_fwd_chunked")
     return out
+
+
+# ------------------------------------------------------- vocabulary loss
+def _vocab_ws(N, H, V, vblock, device):
+    n = ctypes.c_size_t()
+    _check(lib.moe_vocab_loss_workspace_bytes(N, H, V, vblock, ctypes.byref(n)),
+           "moe_vocab_loss_workspace_bytes")
+    return workspace(n.value, device, "vocab_loss")
+
+
+def moe_vocab_loss_fwd(x, w_voc, target, vblock, loss=None, lse=None):
+    """Blockwise online loss of the vocabulary projection.  x [N,H] bf16,
+    w_voc [H,V] bf16, target [N] int32.  Returns (loss [N], lse [N]) fp32."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(w_voc, torch.bfloat16, "w_voc", 2)
+    _need(target, torch.int32, "target", 1)
+    N, H = x.shape
+    V = w_voc.shape[1]
+    if loss is None:
+        loss = torch.empty((N,), dtype=torch.float32, device=x.device)
+    if lse is None:
+        lse = torch.empty((N,), dtype=torch.float32, device=x.device)
+    ws = _vocab_ws(N, H, V, vblock, x.device)
+    _check(lib.moe_vocab_loss_fwd(_ptr(x), _ptr(w_voc), _ptr(target), N, H, V, vblock,
+                                  _ptr(loss), _ptr(lse), _ptr(ws), ws.numel(), _stream()),
+           "moe_vocab_loss_fwd")
+    return loss, lse
+
+
+def moe_vocab_loss_bwd(x, w_voc, target, lse, dloss, vblock, dx=None, dw_voc=None):
+    """Gradients of the vocabulary loss given dloss [N] fp32.  Returns
+    (dx [N,H] bf16, dw_voc [H,V] bf16)."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(w_voc, torch.bfloat16, "w_voc", 2)
+    _need(target, torch.int32, "target", 1)
+    _need(lse, torch.float32, "lse", 1)
+    _need(dloss, torch.float32, "dloss", 1)
+    N, H = x.shape
+    V = w_voc.shape[1]
+    if dx is None:
+        dx = torch.empty((N, H), dtype=torch.bfloat16, device=x.device)
+    if dw_voc is None:
+        dw_voc = torch.empty((H, V), dtype=torch.bfloat16, device=x.device)
+    ws = _vocab_ws(N, H, V, vblock, x.device)
+    _check(lib.moe_vocab_loss_bwd(_ptr(x), _ptr(w_voc), _ptr(target), _ptr(lse), _ptr(dloss), N,
+                                  H, V, vblock, _ptr(dx), _ptr(dw_voc), _ptr(ws), ws.numel(),
+                                  _stream()), "moe_vocab_loss_bwd")
+    return dx, dw_voc
 
 
 # ------------------------------------------------------------- profiling

@@ -112,6 +112,17 @@ Z = None
                                                       P, P, 1 << 20, Z, Z)),
     ("chunked f % 8", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 30, P, P, P, 4,
                                                       P, P, 1 << 20, Z, Z)),
+    ("vocab vblock % 8", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 12, P, P, P, 1 << 30,
+                                                        Z)),
+    ("vocab H % 8", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 60, 100, 16, P, P, P, 1 << 30, Z)),
+    ("vocab V 0", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 64, 0, 16, P, P, P, 1 << 30, Z)),
+    ("vocab N<0", lambda L: L.moe_vocab_loss_fwd(P, P, P, -1, 64, 100, 16, P, P, P, 1 << 30, Z)),
+    ("vocab null lse", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 16, P, Z, P, 1 << 30,
+                                                      Z)),
+    ("vocab bwd null dw", lambda L: L.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, P, Z, P,
+                                                         1 << 30, Z)),
+    ("vocab bwd misaligned dx", lambda L: L.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, MIS,
+                                                               P, P, 1 << 30, Z)),
 ])
 def test_invalid_arguments_rejected_on_host(lib, case):
     name, call = case
@@ -127,6 +138,22 @@ def test_workspace_too_small_rejected(lib):
     assert lib.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, P, Z, Z, 1, Z, P, 16, Z) == -3
     assert lib.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 32, P, P, P, 4, P, P, 16, Z,
                                    Z) == -3
+    assert lib.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
+    assert lib.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
+
+
+def test_vocab_workspace_is_one_block_of_logits():
+    """The vocabulary loss keeps one N x vblock block of logits (fp32, plus
+    its bf16 gradient) and an fp32 dX accumulator, never N x V."""
+    from paper_2607_01844_amd import moe
+    L = moe.lib
+    n1, n2 = ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.moe_vocab_loss_workspace_bytes(4096, 2048, 200000, 16384, ctypes.byref(n1)) == 0
+    assert L.moe_vocab_loss_workspace_bytes(4096, 2048, 400000, 16384, ctypes.byref(n2)) == 0
+    assert n1.value == n2.value  # independent of V
+    base = 4096 * 16384 * 6 + 4096 * 2048 * 4
+    assert base <= n1.value <= base + (33 << 20)
+    assert n1.value < 4096 * 200000 * 4 // 4
 
 
 def test_chunked_workspace_depends_on_chunk_only(lib):

@@ -208,6 +208,46 @@ def make_inputs(wl, seed: int = 0, device="cpu", with_grad: bool = True) -> dict
     return out
 
 
+# --------------------------------------------------------------------------
+# vocabulary projection (Sec. 3.4): X [N,H], W_voc [H,V], targets [N]
+# --------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class VocabWorkload:
+    name: str
+    N: int       # tokens on the device
+    H: int       # model width
+    V: int       # vocabulary size
+    vblock: int  # vocabulary columns per block of the online loss
+
+    def describe(self) -> str:
+        return f"{self.name}: N={self.N} H={self.H} V={self.V} vblock={self.vblock}"
+
+
+# The paper's size example is V = 2e5; the mid workload uses it with the MoE
+# mid layer's N and H.  The tiny one has a ragged last block.
+VOCAB_WORKLOADS = {
+    "vocab_tiny": VocabWorkload("vocab_tiny", N=256, H=128, V=1000, vblock=256),
+    "vocab_mid": VocabWorkload("vocab_mid", N=4096, H=2048, V=200000, vblock=16384),
+}
+
+
+def make_vocab_inputs(vw: VocabWorkload, seed: int = 0, device="cpu") -> dict:
+    """x ~ N(0,1) bf16 [N,H]; w_voc ~ N(0, 0.02) bf16 [H,V]; target uniform
+    on [0, V) int32 [N]; dloss ~ N(0,1) fp32 [N] (an arbitrary upstream
+    gradient, so both signs occur).  Draw order: x, w_voc, target, dloss."""
+    dev = torch.device(device)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    out = {"workload": vw}
+    out["x"] = _normal((vw.N, vw.H), 1.0, gen, dev, torch.bfloat16)
+    out["w_voc"] = _normal((vw.H, vw.V), W_STD, gen, dev, torch.bfloat16)
+    out["target"] = torch.randint(0, vw.V, (vw.N,), generator=gen, device=dev,
+                                  dtype=torch.int64).to(torch.int32)
+    out["dloss"] = _normal((vw.N,), 1.0, gen, dev, torch.float32)
+    return out
+
+
 def bf16_bits(t: torch.Tensor) -> np.ndarray:
     """uint16 view of a bf16 tensor's bits, on the host."""
     assert t.dtype == torch.bfloat16
