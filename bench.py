@@ -201,6 +201,49 @@ def chunked_forward(layer, steps: int):
     return out
 
 
+def vendor_batched(wl, steps: int):
+    """Context, not part of the path: the vendor library's batched GEMM
+    (torch.bmm, bf16, contiguous operands) on the same six products with
+    every local expert holding exactly T*k/E rows — the uniform, padded-free
+    special case a batched GEMM can express.  Per product: microseconds and
+    TFLOP/s."""
+    E, n, d, f = wl.E_loc, wl.T * wl.k // wl.E, wl.d, wl.f
+    g = torch.Generator(device="cuda").manual_seed(1)
+
+    def rnd(*shape, std=1.0):
+        return (std * torch.randn(shape, generator=g, device="cuda")).to(torch.bfloat16)
+    x, dy = rnd(E, n, d), rnd(E, n, d)
+    a, dh = rnd(E, n, f), rnd(E, n, 2 * f)
+    w_gu, w_d = rnd(E, d, 2 * f, std=0.02), rnd(E, f, d, std=0.02)
+    w_dT, w_guT = w_d.transpose(1, 2).contiguous(), w_gu.transpose(1, 2).contiguous()
+    xT, aT = x.transpose(1, 2).contiguous(), a.transpose(1, 2).contiguous()
+    prods = {
+        "fwd_gate_up": (x, w_gu, 4.0), "fwd_down": (a, w_d, 2.0),
+        "dgrad_down": (dy, w_dT, 2.0), "dgrad_gate_up": (dh, w_guT, 4.0),
+        "wgrad_gate_up": (xT, dh, 4.0), "wgrad_down": (aT, dy, 2.0),
+    }
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out, total_ms = {}, 0.0
+    for name, (lhs, rhs, c) in prods.items():
+        res = torch.empty((E, lhs.shape[1], rhs.shape[2]), dtype=torch.bfloat16, device="cuda")
+        torch.bmm(lhs, rhs, out=res)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            torch.bmm(lhs, rhs, out=res)
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / steps
+        total_ms += ms
+        fl = c * E * n * d * f
+        out[name] = {"us": round(ms * 1e3, 1), "tflops": round(fl / (ms * 1e-3) / 1e12, 1)}
+        del res
+    out["all_six"] = {"us": round(total_ms * 1e3, 1),
+                      "tflops": round(18.0 * E * n * d * f / (total_ms * 1e-3) / 1e12, 1)}
+    out["rows_per_expert"] = n
+    return out
+
+
 def vocab_loss(steps: int, warmup: int):
     """Blockwise vocabulary loss on its own workload (Sec. 3.4): forward,
     backward and both, with the dense-equivalent FLOP rate (2NHV forward,
@@ -291,6 +334,8 @@ def main():
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--no-vocab", action="store_true", help="skip the vocabulary-loss leg")
+    ap.add_argument("--no-vendor", action="store_true",
+                    help="skip the vendor batched-GEMM context measurement")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
@@ -374,6 +419,11 @@ def main():
     memfwd = chunked_forward(layer, args.steps)
     log(f"[bench] memory-efficient forward: {memfwd}")
 
+    vendor = None
+    if not args.no_vendor:
+        vendor = vendor_batched(wl, args.steps)
+        log(f"[bench] vendor batched GEMM (uniform rows, context): {vendor['all_six']}")
+
     voc = None
     if not args.no_vocab:
         del layer
@@ -401,6 +451,7 @@ def main():
                                  "value": round(wl.T / (ms_rb * 1e-3), 1), "unit": "tokens/s"},
         "memory_efficient_forward": memfwd,
         "vocab_loss": voc,
+        "vendor_batched_gemm_context": vendor,
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,
