@@ -244,6 +244,60 @@ def vendor_batched(wl, steps: int):
     return out
 
 
+def llep_leg(steps: int, E_p: int = 8, name: str = "large_skew"):
+    """Least-loaded expert parallelism on one GPU's view of E_p ranks
+    (Sec. 3.3): the skewed workload's real routing, the plan, and the
+    forward expert GEMMs of every rank under standard expert parallelism
+    (each rank its own E/E_p experts) and under the plan.  The slowest rank
+    sets the layer's pace on E_p GPUs; the plan and the dispatch are timed
+    too."""
+    from paper_2607_01844_amd import moe as m
+    wl = W.WORKLOADS[name]
+    inp = W.make_inputs(wl, seed=0, device="cuda", with_grad=False)
+    E, G = wl.E, wl.E // E_p
+    idx, gate = m.moe_route(inp["x"], inp["w_router"], inp.get("router_bias"), wl.k, wl.renorm)
+    pm = m.moe_permute(inp["x"], idx, E, 0, E)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, n=steps):
+        fn()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(n):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / n
+
+    plan = {}
+    plan_ms = timed(lambda: plan.update(zip(("lo", "hi", "load", "ns"),
+                                            m.moe_llep_plan(pm["counts_global"], E_p))))
+    counts = pm["counts_global"].cpu().numpy()
+    ep_load = counts.reshape(E_p, G).sum(axis=1)
+    cap_ep, cap_ll = int(ep_load.max()), -(-wl.T * wl.k // E_p)
+    w = (inp["w_gate"], inp["w_up"], inp["w_down"])
+    ep_ms, ll_ms, disp_ms = [], [], []
+    for r in range(E_p):
+        sl = slice(r * G, (r + 1) * G)
+        pr = m.moe_permute(inp["x"], idx, E, r * G, G, cap=cap_ep)
+        ws = tuple(t[sl] for t in w)
+        ep_ms.append(timed(lambda: m.moe_grouped_swiglu_fwd(pr["x_perm"], pr["expert_offsets"],
+                                                            *ws, cap=cap_ep)))
+        box = {}
+        disp_ms.append(timed(lambda: box.update(m.moe_llep_dispatch(
+            inp["x"], idx, pm["expert_offsets"], pm["dst"], plan["lo"], plan["hi"], r, cap_ll))))
+        ll_ms.append(timed(lambda: m.moe_grouped_swiglu_fwd(box["x_perm"], box["expert_offsets"],
+                                                            *w, cap=cap_ll)))
+    load = plan["load"].cpu().numpy()
+    return {"workload": f"{name} routing, E_p={E_p} ranks of {G} experts",
+            "standard_ep_rank_rows": ep_load.tolist(), "llep_rank_rows": load.tolist(),
+            "weight_shipments": int(plan["ns"].item()),
+            "standard_ep_slowest_rank_fwd_gemm_ms": round(max(ep_ms), 4),
+            "llep_slowest_rank_fwd_gemm_ms": round(max(ll_ms), 4),
+            "straggler_speedup": round(max(ep_ms) / max(ll_ms), 3),
+            "plan_ms": round(plan_ms, 4), "dispatch_ms_per_rank": round(float(np.mean(disp_ms)), 4)}
+
+
 def vocab_loss(steps: int, warmup: int):
     """Blockwise vocabulary loss on its own workload (Sec. 3.4): forward,
     backward and both, with the dense-equivalent FLOP rate (2NHV forward,
@@ -313,10 +367,14 @@ def cpu_baseline(wl, inp, budget_s: float):
                      prec="f32")
         return time.perf_counter() - t0
 
-    probe_t = 32
-    dt = run(probe_t)
-    ts = int(min(wl.T, max(probe_t, probe_t * budget_s / max(dt, 1e-3))))
-    dt = run(ts)
+    # the cost per token grows with the sample (more tokens per expert), so
+    # the size is re-estimated from the last run until it fills the budget
+    ts, dt = 32, run(32)
+    for _ in range(3):
+        if ts >= wl.T or dt >= 0.6 * budget_s:
+            break
+        ts = int(min(wl.T, max(ts + 1, ts * budget_s / max(dt, 1e-3))))
+        dt = run(ts)
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": round(ts / dt, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"fp32 oracle fwd+bwd (routing, permutation, expert FFN, combine, all "
@@ -334,6 +392,8 @@ def main():
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--no-vocab", action="store_true", help="skip the vocabulary-loss leg")
+    ap.add_argument("--no-llep", action="store_true",
+                    help="skip the least-loaded expert-parallelism leg")
     ap.add_argument("--no-vendor", action="store_true",
                     help="skip the vendor batched-GEMM context measurement")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -424,10 +484,16 @@ def main():
         vendor = vendor_batched(wl, args.steps)
         log(f"[bench] vendor batched GEMM (uniform rows, context): {vendor['all_six']}")
 
+    del layer
+    torch.cuda.empty_cache()
+    llep = None
+    if not args.no_llep:
+        llep = llep_leg(args.steps)
+        log(f"[bench] least-loaded expert parallelism: {llep}")
+        torch.cuda.empty_cache()
+
     voc = None
     if not args.no_vocab:
-        del layer
-        torch.cuda.empty_cache()
         voc = vocab_loss(args.steps, args.warmup)
         log(f"[bench] vocabulary loss: {voc}")
 
@@ -450,6 +516,7 @@ def main():
         "with_router_backward": {"ms_per_step": round(ms_rb, 4),
                                  "value": round(wl.T / (ms_rb * 1e-3), 1), "unit": "tokens/s"},
         "memory_efficient_forward": memfwd,
+        "llep": llep,
         "vocab_loss": voc,
         "vendor_batched_gemm_context": vendor,
         "roofline": roof,

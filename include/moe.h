@@ -49,6 +49,7 @@ extern "C" {
 #define MOE_ABI_VERSION 1
 #define MOE_MAX_K 16
 #define MOE_MAX_E 1024
+#define MOE_LLEP_MAX_RANKS 64
 
 typedef uint16_t moe_bf16;
 
@@ -277,6 +278,56 @@ int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* 
                        const float* lse, const float* dloss, int64_t N, int H, int64_t V,
                        int64_t vblock, moe_bf16* dx, moe_bf16* dw_voc, void* workspace,
                        size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------ least-loaded expert parallelism
+ * Sec. 3.3 (recap of LLEP): at every MoE call the per-rank load is
+ * measured, excess token-expert assignments move from overloaded ranks to
+ * underloaded ones and the expert weights travel with them, so that the
+ * receiving rank computes those products itself; which products are
+ * computed never changes.  The planning steps are not given in the paper;
+ * this library's plan is:
+ *   - E experts on E_p ranks, expert e at home on rank e / (E / E_p);
+ *     L = sum of counts; capacity C = max(capacity, ceil(L / E_p));
+ *   - every rank keeps its own experts, ascending, while its load stays
+ *     <= C; the rest of an expert is its spill;
+ *   - experts with spill, largest spill first (ties: lower index), hand it
+ *     out in pieces, each to the currently least loaded rank (ties: lower
+ *     rank) and as large as that rank's room below C.
+ * Expert e's assignments in the layer's row order (ascending t*k + i, the
+ * order of moe_permute) are cut into consecutive windows: the home rank's
+ * [0, keep) first, then the pieces in the order handed out.  Every rank's
+ * load is <= C; a piece on a rank other than the home is one shipment of
+ * that expert's weights.
+ *
+ * moe_llep_plan: counts [E] int32 (assignments per expert over all tokens,
+ * e.g. moe_permute's counts_global) -> win_lo, win_hi [E_p][E] int32 (rank
+ * r computes rows [win_lo[r][e], win_hi[r][e]) of expert e; empty windows
+ * are [0, 0)), load [E_p] int32, n_ship [1] int32.  One workgroup, all on
+ * the device (no host round trip for the counts).  Limits: 1 <= E_p <=
+ * MOE_LLEP_MAX_RANKS, E a multiple of E_p, capacity >= 0.
+ *
+ * moe_llep_dispatch: one rank's share of the layer under a plan.  Inputs:
+ * x [T][d], topk_idx [T][k], and the permutation of ALL experts from
+ * moe_permute(expert_begin = 0, num_local = E): offsets_all [E + 1] and
+ * dst_all [T*k]; the plan (win_lo, win_hi, E_p) and the rank.  Outputs, in
+ * the moe_permute layout over all E experts: offsets_r [E + 1] (expert e's
+ * rows at [offsets_r[e], offsets_r[e + 1]), clamped to cap), row_src_r
+ * [cap], dst_r [T*k] (-1 for assignments other ranks compute) and x_perm_r
+ * [cap][d].  cap must be >= the rank's load, which the plan bounds by
+ * max(capacity, ceil(T*k / E_p)); rows past cap are dropped.  The rank then
+ * runs moe_grouped_swiglu_fwd/_bwd with num_local = E on these buffers (a
+ * shipped expert's weights are read from the [E] weight arrays) and
+ * moe_combine into its partial output; the partial outputs of all ranks
+ * sum to the layer's output, and every y_perm row equals the one the whole
+ * layer computes for that assignment.
+ */
+int moe_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* win_lo,
+                  int32_t* win_hi, int32_t* load, int32_t* n_ship, void* stream);
+int moe_llep_dispatch(const moe_bf16* x, const int32_t* topk_idx, const int32_t* offsets_all,
+                      const int32_t* dst_all, const int32_t* win_lo, const int32_t* win_hi,
+                      int E_p, int rank, int64_t T, int d, int E, int k, int64_t cap,
+                      int32_t* offsets_r, int32_t* row_src_r, int32_t* dst_r, moe_bf16* x_perm_r,
+                      void* stream);
 
 /* ------------------------------------------------------------- profiling
  * Optional per-kernel timing with HIP events recorded on the launch stream

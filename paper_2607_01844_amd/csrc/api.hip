@@ -87,7 +87,7 @@ const char* const kNames[moe::K_NUM] = {
     "permute_rank", "permute_gather",  "gemm_sched",         "gemm_fwd_gate_up",
     "gemm_fwd_down", "gemm_dgrad_down", "gemm_dgrad_gate_up", "gemm_wgrad_gate_up",
     "gemm_wgrad_down", "combine",       "combine_bwd",        "route_dlogits",
-    "route_dw",     "route_dx",        "vocab_lse",          "vocab_grad"};
+    "route_dw",     "route_dx",        "vocab_lse",          "vocab_grad",    "llep_plan",     "llep_window"};
 
 }  // namespace
 
@@ -441,6 +441,45 @@ MOE_API int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const i
   }
   return hip_status(moe::launch_vocab_bwd(x, w_voc, target, lse, dloss, N, H, V, vblock, dx,
                                           dw_voc, workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// ------------------------------------------------ least-loaded expert parallelism
+MOE_API int moe_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* win_lo,
+                          int32_t* win_hi, int32_t* load, int32_t* n_ship, void* stream) {
+  const char* fn = "moe_llep_plan";
+  CHECK(E >= 1 && E <= MOE_MAX_E, "E out of [1, MOE_MAX_E]");
+  CHECK(E_p >= 1 && E_p <= MOE_LLEP_MAX_RANKS, "E_p out of [1, MOE_LLEP_MAX_RANKS]");
+  CHECK(E % E_p == 0, "E must be a multiple of E_p");
+  CHECK(capacity >= 0, "capacity < 0");
+  REQ(counts); REQ(win_lo); REQ(win_hi); REQ(load); REQ(n_ship);
+  return hip_status(moe::launch_llep_plan(counts, E, E_p, capacity, win_lo, win_hi, load, n_ship,
+                                          static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+MOE_API int moe_llep_dispatch(const moe_bf16* x, const int32_t* topk_idx,
+                              const int32_t* offsets_all, const int32_t* dst_all,
+                              const int32_t* win_lo, const int32_t* win_hi, int E_p, int rank,
+                              int64_t T, int d, int E, int k, int64_t cap, int32_t* offsets_r,
+                              int32_t* row_src_r, int32_t* dst_r, moe_bf16* x_perm_r,
+                              void* stream) {
+  const char* fn = "moe_llep_dispatch";
+  if (int r = check_tk(fn, T, E, k)) return r;
+  if (int r = check_dim(fn, d, "d")) return r;
+  CHECK(E_p >= 1 && E_p <= MOE_LLEP_MAX_RANKS && E % E_p == 0,
+        "E_p out of [1, MOE_LLEP_MAX_RANKS] or not a divisor of E");
+  CHECK(rank >= 0 && rank < E_p, "rank out of [0, E_p)");
+  CHECK(cap >= 0 && cap <= T * k, "cap out of [0, T*k]");
+  REQ(offsets_all); REQ(win_lo); REQ(win_hi); REQ(offsets_r);
+  if (T > 0) {
+    REQ(x); REQ(topk_idx); REQ(dst_all); REQ(dst_r);
+    if (cap > 0) { REQ(row_src_r); REQ(x_perm_r); }
+  }
+  const int64_t o = static_cast<int64_t>(rank) * E;
+  return hip_status(moe::launch_llep_dispatch(x, topk_idx, offsets_all, dst_all, win_lo + o,
+                                              win_hi + o, T, d, E, k, cap, offsets_r, row_src_r,
+                                              dst_r, x_perm_r, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

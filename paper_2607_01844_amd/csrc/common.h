@@ -85,6 +85,8 @@ enum KernelId {
   K_ROUTE_DX,
   K_VOC_LSE,
   K_VOC_GRAD,
+  K_LLEP_PLAN,
+  K_LLEP_WINDOW,
   K_NUM
 };
 
@@ -126,6 +128,15 @@ hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int 
                           int e_begin, int E_loc, int32_t* offsets, int32_t* counts_global,
                           int32_t* row_src, int32_t* dst, uint16_t* x_perm, void* ws,
                           hipStream_t s);
+hipError_t launch_gather(const uint16_t* x, const int32_t* dst, int64_t T, int d, int k,
+                         uint16_t* x_perm, hipStream_t s);
+hipError_t launch_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* lo,
+                            int32_t* hi, int32_t* load, int32_t* n_ship, hipStream_t s);
+hipError_t launch_llep_dispatch(const uint16_t* x, const int32_t* idx, const int32_t* offsets_all,
+                                const int32_t* dst_all, const int32_t* lo, const int32_t* hi,
+                                int64_t T, int d, int E, int k, int64_t cap, int32_t* offsets_r,
+                                int32_t* row_src_r, int32_t* dst_r, uint16_t* x_perm_r,
+                                hipStream_t s);
 hipError_t launch_combine(const uint16_t* y, const int32_t* dst, const float* gate, int64_t T,
                           int d, int k, uint16_t* out, hipStream_t s);
 hipError_t launch_combine_bwd(const uint16_t* dout, const uint16_t* y, const int32_t* dst,

@@ -251,4 +251,14 @@ hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int 
   return hipGetLastError();
 }
 
+hipError_t launch_gather(const uint16_t* x, const int32_t* dst, int64_t T, int d, int k,
+                         uint16_t* x_perm, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  prof_begin(K_PERM_GATHER, s);
+  perm_gather_kernel<<<static_cast<unsigned>(ceil_div(T, 4)), 256, 0, s>>>(x, dst, T, d, k,
+                                                                           x_perm);
+  prof_end(K_PERM_GATHER, s);
+  return hipGetLastError();
+}
+
 }  // namespace moe

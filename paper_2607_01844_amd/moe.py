@@ -31,6 +31,7 @@ C_SYMBOLS = (
     "moe_combine", "moe_combine_bwd",
     "moe_ffn_fwd_chunked_workspace_bytes", "moe_ffn_fwd_chunked",
     "moe_vocab_loss_workspace_bytes", "moe_vocab_loss_fwd", "moe_vocab_loss_bwd",
+    "moe_llep_plan", "moe_llep_dispatch",
     "moe_profile_enable", "moe_profile_reset", "moe_profile_num_kernels",
     "moe_profile_kernel_name", "moe_profile_query",
 )
@@ -69,6 +70,8 @@ def _load():
         "moe_vocab_loss_workspace_bytes": ([I64, I, I64, I64, PSZ], I),
         "moe_vocab_loss_fwd": ([P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
         "moe_vocab_loss_bwd": ([P, P, P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
+        "moe_llep_plan": ([P, I, I, I, P, P, P, P, P], I),
+        "moe_llep_dispatch": ([P, P, P, P, P, P, I, I, I64, I, I, I, I64, P, P, P, P, P], I),
         "moe_profile_enable": ([I], I),
         "moe_profile_reset": ([], I),
         "moe_profile_num_kernels": ([], I),
@@ -391,6 +394,48 @@ def moe_vocab_loss_bwd(x, w_voc, target, lse, dloss, vblock, dx=None, dw_voc=Non
                                   H, V, vblock, _ptr(dx), _ptr(dw_voc), _ptr(ws), ws.numel(),
                                   _stream()), "moe_vocab_loss_bwd")
     return dx, dw_voc
+
+
+# ------------------------------------------ least-loaded expert parallelism
+def moe_llep_plan(counts, E_p, capacity=0):
+    """Plan of which rank computes which rows of every expert.  counts [E]
+    int32 (device).  Returns (win_lo [E_p,E], win_hi [E_p,E], load [E_p],
+    n_ship [1]), int32 device tensors."""
+    _need(counts, torch.int32, "counts", 1)
+    E = counts.shape[0]
+    dev = counts.device
+    lo = torch.empty((E_p, E), dtype=torch.int32, device=dev)
+    hi = torch.empty((E_p, E), dtype=torch.int32, device=dev)
+    load = torch.empty((E_p,), dtype=torch.int32, device=dev)
+    n_ship = torch.empty((1,), dtype=torch.int32, device=dev)
+    _check(lib.moe_llep_plan(_ptr(counts), E, E_p, capacity, _ptr(lo), _ptr(hi), _ptr(load),
+                             _ptr(n_ship), _stream()), "moe_llep_plan")
+    return lo, hi, load, n_ship
+
+
+def moe_llep_dispatch(x, topk_idx, offsets_all, dst_all, win_lo, win_hi, rank, cap):
+    """Rank `rank`'s rows under a plan, from the all-expert permutation.
+    Returns {expert_offsets [E+1], row_src [cap], dst [T,k], x_perm [cap,d]}."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(topk_idx, torch.int32, "topk_idx", 2)
+    _need(offsets_all, torch.int32, "offsets_all", 1)
+    _need(dst_all, torch.int32, "dst_all")
+    _need(win_lo, torch.int32, "win_lo", 2)
+    _need(win_hi, torch.int32, "win_hi", 2)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    E_p, E = win_lo.shape
+    dev = x.device
+    out = {"expert_offsets": torch.empty((E + 1,), dtype=torch.int32, device=dev),
+           "row_src": torch.empty((max(cap, 1),), dtype=torch.int32, device=dev),
+           "dst": torch.empty((T, k), dtype=torch.int32, device=dev),
+           "x_perm": torch.empty((max(cap, 1), d), dtype=torch.bfloat16, device=dev)}
+    _check(lib.moe_llep_dispatch(_ptr(x), _ptr(topk_idx), _ptr(offsets_all), _ptr(dst_all),
+                                 _ptr(win_lo), _ptr(win_hi), E_p, rank, T, d, E, k, cap,
+                                 _ptr(out["expert_offsets"]), _ptr(out["row_src"]),
+                                 _ptr(out["dst"]), _ptr(out["x_perm"]), _stream()),
+           "moe_llep_dispatch")
+    return out
 
 
 # ------------------------------------------------------------- profiling

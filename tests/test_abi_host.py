@@ -123,6 +123,16 @@ Z = None
                                                          1 << 30, Z)),
     ("vocab bwd misaligned dx", lambda L: L.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, MIS,
                                                                P, P, 1 << 30, Z)),
+    ("llep E_p > max", lambda L: L.moe_llep_plan(P, 128, 128, 0, P, P, P, P, Z)),
+    ("llep E % E_p", lambda L: L.moe_llep_plan(P, 12, 5, 0, P, P, P, P, Z)),
+    ("llep capacity < 0", lambda L: L.moe_llep_plan(P, 12, 4, -1, P, P, P, P, Z)),
+    ("llep null load", lambda L: L.moe_llep_plan(P, 12, 4, 0, P, P, Z, P, Z)),
+    ("llep dispatch rank", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 4, 4, 10, 64, 12, 2, 5,
+                                                         P, P, P, P, Z)),
+    ("llep dispatch cap", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 4, 0, 10, 64, 12, 2, 21,
+                                                        P, P, P, P, Z)),
+    ("llep dispatch E_p", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 5, 0, 10, 64, 12, 2, 5,
+                                                        P, P, P, P, Z)),
 ])
 def test_invalid_arguments_rejected_on_host(lib, case):
     name, call = case

@@ -248,6 +248,19 @@ def make_vocab_inputs(vw: VocabWorkload, seed: int = 0, device="cpu") -> dict:
     return out
 
 
+def make_topk(T: int, k: int, E: int, zipf_s: float, seed: int = 0) -> np.ndarray:
+    """Synthetic routing (no router): for every token k distinct experts,
+    drawn without replacement with probabilities proportional to
+    rank^-zipf_s over a seeded random ranking of the experts (Gumbel top-k).
+    Returns int32 [T, k].  zipf_s = 0 is uniform."""
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(E)
+    logp = np.empty(E)
+    logp[order] = -zipf_s * np.log(np.arange(1, E + 1))
+    g = rng.gumbel(size=(T, E))
+    return np.argsort(-(logp[None, :] + g), axis=1, kind="stable")[:, :k].astype(np.int32)
+
+
 def bf16_bits(t: torch.Tensor) -> np.ndarray:
     """uint16 view of a bf16 tensor's bits, on the host."""
     assert t.dtype == torch.bfloat16
