@@ -410,6 +410,10 @@ def main():
     log(f"[bench] workload {wl.describe()}")
     inp = W.make_inputs(wl, seed=0, device="cuda")
     layer = Layer(wl, inp)
+    # the router backward's first call creates the device's rocBLAS handle
+    # (a few hundred ms, once per process): outside every timed region
+    layer.step()
+    layer.router_bwd()
     for _ in range(args.warmup):
         layer.step()
     torch.cuda.synchronize()

@@ -21,7 +21,7 @@ LIB = os.path.join(PKG, "libmoe.so")
 # object), written beside the library at every build: a stored measurement
 # names the code it was taken on, and stays valid while that code is unchanged
 DEVICE_TEXT = os.path.join(PKG, "libmoe.device_text.json")
-SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "chunked.hip", "vocab.hip", "llep.hip"]
+SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "chunked.hip", "vocab.hip", "llep.hip", "blas.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -3,13 +3,19 @@
 //   gate gradients -> logit gradients (softmax Jacobian at the chosen slots)
 //   -> dW_r = x^T dlogits, dbias = column sums of dlogits,
 //      dx_router = dlogits W_r^T  (added to the expert path's dx).
-// Everything is fp32 with fixed summation orders, so results are bitwise
-// reproducible.  The two contractions are tiny next to the expert GEMMs
-// (2 T d E FLOP each) and stay on the fp32 vector ALUs: no bf16 rounding of
-// dlogits, which would cost the router gradient its precision.
+// Fixed summation orders throughout, so results are bitwise reproducible.
+// The two contractions (2 T d E FLOP each) run on the fp32 vector ALUs when
+// they are small.  Large ones (a trillion-scale share: T = 16384, d = 7168,
+// E = 384) go to the bf16 matrix cores without losing fp32 precision: every
+// fp32 operand v is split into bf16 hi = bf16(v) and lo = bf16(v - hi)
+// (|v - hi - lo| <= 2^-17 |v|), and the products are taken as
+//   dW_r = x^T (hi + lo)        (x is exactly bf16),
+//   dx_router = hi_d hi_w + hi_d lo_w + lo_d hi_w
+// with fp32 accumulation (rocBLAS products, atomics off; the token range of
+// dW_r is cut into chunks whose partial sums are added in chunk order).
 #include <algorithm>
 
-#include "common.h"
+#include "blas.h"
 
 namespace moe {
 namespace {
@@ -183,6 +189,53 @@ __global__ __launch_bounds__(256) void route_dw_reduce_kernel(const float* __res
   }
 }
 
+// hi / lo bf16 parts of fp32 values: dst row r gets, for each of its E
+// source values v, the parts in the column groups `order` names (0 = hi,
+// 1 = lo), so that one product over 3E columns sums the three cross terms.
+__device__ __forceinline__ void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
+  hi = static_cast<uint16_t>(f32_to_bf16_bits(v));
+  lo = static_cast<uint16_t>(f32_to_bf16_bits(v - bf16_to_f32(hi)));
+}
+// dl [T][E] -> b3 [T][3E] = [hi | hi | lo]
+__global__ __launch_bounds__(256) void route_split_dl_kernel(const float* __restrict__ dl,
+                                                             int64_t n, int E,
+                                                             uint16_t* __restrict__ b3) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int64_t t = i / E, e = i - t * E;
+  uint16_t hi, lo;
+  split_bf16(dl[i], hi, lo);
+  uint16_t* row = b3 + t * 3 * E;
+  row[e] = hi;
+  row[E + e] = hi;
+  row[2 * E + e] = lo;
+}
+// W_r [d][E] -> a3 [d][3E] = [hi | lo | hi]
+__global__ __launch_bounds__(256) void route_split_w_kernel(const float* __restrict__ w, int64_t n,
+                                                            int E, uint16_t* __restrict__ a3) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int64_t j = i / E, e = i - j * E;
+  uint16_t hi, lo;
+  split_bf16(w[i], hi, lo);
+  uint16_t* row = a3 + j * 3 * E;
+  row[e] = hi;
+  row[E + e] = lo;
+  row[2 * E + e] = hi;
+}
+// bpart[c][e] = sum over the tokens of chunk c, ascending, of dl[t][e]
+__global__ __launch_bounds__(256) void route_dbias_part_kernel(const float* __restrict__ dl,
+                                                               int64_t T, int E, int64_t chunk,
+                                                               float* __restrict__ bpart) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int c = blockIdx.y;
+  if (e >= E) return;
+  const int64_t t0 = c * chunk, t1 = std::min(T, t0 + chunk);
+  float acc = 0.0f;
+  for (int64_t t = t0; t < t1; ++t) acc += dl[t * E + e];
+  bpart[static_cast<int64_t>(c) * E + e] = acc;
+}
+
 // dx[t][j] = bf16( [float(dx[t][j]) +] sum over e ascending of dl[t][e] * W_r[j][e] ).
 // Block = 64 tokens x 64 hidden columns, thread = 4 tokens x 4 columns; dl
 // and W_r are staged transposed (expert-major) 32 experts at a time.
@@ -259,15 +312,113 @@ int route_bwd_chunks(int64_t T, int d, int E) {
   return static_cast<int>(std::max<int64_t>(1, std::min(want, most)));
 }
 
+namespace {
+// the matrix-core path takes contractions of at least 2^28 multiply-adds
+bool route_bwd_mfma(int64_t T, int d, int E) {
+  return T * static_cast<int64_t>(d) * E >= (int64_t{1} << 28);
+}
+// matrix-core path: token chunks of dW_r, so that the products have about
+// 512 output tiles of 256 x 256 between them
+int route_bwd_mfma_chunks(int64_t T, int d, int E) {
+  const int64_t tiles = ceil_div(d, 256) * ceil_div(E, 256);
+  return static_cast<int>(std::max<int64_t>(1, std::min(ceil_div(512, tiles), ceil_div(T, 256))));
+}
+}  // namespace
+
 size_t route_bwd_ws_bytes(int64_t T, int d, int E) {
-  const int S = route_bwd_chunks(T, d, E);
+  const bool mf = route_bwd_mfma(T, d, E);
+  const int S = mf ? route_bwd_mfma_chunks(T, d, E) : route_bwd_chunks(T, d, E);
   size_t b = align_up(sizeof(float) * static_cast<size_t>(T) * E, 256);  // dlogits
   if (S > 1) {
     b += align_up(sizeof(float) * static_cast<size_t>(S) * d * E, 256);  // dW_r partials
     b += align_up(sizeof(float) * static_cast<size_t>(S) * E, 256);      // bias partials
   }
+  if (mf) {
+    b += align_up(sizeof(uint16_t) * static_cast<size_t>(T) * 3 * E, 256);  // dl parts
+    b += align_up(sizeof(uint16_t) * static_cast<size_t>(d) * 3 * E, 256);  // W_r parts
+    b += kBlasWs;
+  }
   return b;
 }
+
+namespace {
+// dW_r, dbias and dx from the logit gradients on the matrix cores (see the
+// top of the file); p = the workspace past the dlogits buffer
+hipError_t launch_route_bwd_mfma(const uint16_t* x, const float* w, int64_t T, int d, int E,
+                                 const float* dl, float* dw, float* dbias, uint16_t* dx,
+                                 int dx_accumulate, char* p, hipStream_t s) {
+  const int64_t chunk = ceil_div(T, route_bwd_mfma_chunks(T, d, E));
+  const int S = static_cast<int>(ceil_div(T, chunk));  // chunks that hold tokens
+  const int64_t nw = static_cast<int64_t>(d) * E;
+  const int E3 = 3 * E;
+  float* part = dw;
+  float* bpart = nullptr;
+  if (S > 1) {
+    part = reinterpret_cast<float*>(p);
+    p += align_up(sizeof(float) * static_cast<size_t>(S) * nw, 256);
+    bpart = reinterpret_cast<float*>(p);
+    p += align_up(sizeof(float) * static_cast<size_t>(S) * E, 256);
+  }
+  uint16_t* b3 = reinterpret_cast<uint16_t*>(p);
+  p += align_up(sizeof(uint16_t) * static_cast<size_t>(T) * E3, 256);
+  uint16_t* a3 = reinterpret_cast<uint16_t*>(p);
+  p += align_up(sizeof(uint16_t) * static_cast<size_t>(d) * E3, 256);
+  void* bws = p;
+
+  prof_begin(K_ROUTE_DW, s);
+  route_split_dl_kernel<<<static_cast<unsigned>(ceil_div(T * E, 256)), 256, 0, s>>>(dl, T * E, E,
+                                                                                   b3);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  if (dbias != nullptr) {
+    route_dbias_part_kernel<<<dim3(static_cast<unsigned>(ceil_div(E, 256)),
+                                   static_cast<unsigned>(S)),
+                              256, 0, s>>>(dl, T, E, chunk, S > 1 ? bpart : dbias);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  }
+  {
+    BlasLease B(s, bws);
+    if (hipError_t e = B.status(); e != hipSuccess) return e;
+    // chunk c of tokens: part_c (col-major E x d = row-major [d][E]) =
+    // (hi + lo)_c (col-major E x chunk, columns of b3) x_c^T, full chunks in
+    // one batched product, the shorter last chunk on its own
+    const int64_t nfull = T / chunk, tail = T - nfull * chunk;
+    for (int pass = 0; pass < 2; ++pass) {
+      const uint16_t* A = b3 + (pass ? 2 * E : 0);
+      const float beta = pass ? 1.0f : 0.0f;
+      if (nfull > 0)
+        if (hipError_t e = gemm_bf16(B.handle(), false, true, E, d, static_cast<int>(chunk), A, E3,
+                                     chunk * E3, x, d, chunk * d, beta, part, false, E, nw,
+                                     static_cast<int>(nfull));
+            e != hipSuccess)
+          return e;
+      if (tail > 0)
+        if (hipError_t e = gemm_bf16(B.handle(), false, true, E, d, static_cast<int>(tail),
+                                     A + nfull * chunk * E3, E3, 0, x + nfull * chunk * d, d, 0,
+                                     beta, part + nfull * nw, false, E, 0);
+            e != hipSuccess)
+          return e;
+    }
+    if (S > 1) {
+      const int nb = dbias ? E : 0;
+      route_dw_reduce_kernel<<<static_cast<unsigned>(ceil_div(nw + nb, 256)), 256, 0, s>>>(
+          part, nw, S, dw, bpart, nb, dbias);
+      if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    }
+    prof_end(K_ROUTE_DW, s);
+    if (dx == nullptr) return hipSuccess;
+    prof_begin(K_ROUTE_DX, s);
+    route_split_w_kernel<<<static_cast<unsigned>(ceil_div(nw, 256)), 256, 0, s>>>(w, nw, E, a3);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    // dx (col-major d x T) [+]= a3^T (d x 3E) b3 (3E x T), rounded to bf16 once
+    if (hipError_t e = gemm_bf16(B.handle(), true, false, d, static_cast<int>(T), E3, a3, E3, 0,
+                                 b3, E3, 0, dx_accumulate ? 1.0f : 0.0f, dx, true, d, 0);
+        e != hipSuccess)
+      return e;
+    prof_end(K_ROUTE_DX, s);
+  }
+  return hipSuccess;
+}
+}  // namespace
 
 hipError_t launch_route_bwd(const uint16_t* x, const float* w, const float* logits,
                             const int32_t* idx, const float* gate, const float* dgate,
@@ -302,6 +453,8 @@ hipError_t launch_route_bwd(const uint16_t* x, const float* w, const float* logi
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
 
+  if (route_bwd_mfma(T, d, E))
+    return launch_route_bwd_mfma(x, w, T, d, E, dl, dw, dbias, dx, dx_accumulate, p, s);
   const int S = route_bwd_chunks(T, d, E);
   const int64_t chunk = ceil_div(T, S);
   float* part = dw;

@@ -10,16 +10,10 @@
 //
 // The three products per block are plain dense GEMMs and go to rocBLAS (bf16
 // operands, fp32 accumulation); everything between them is the kernels here.
-#include <rocblas/rocblas.h>
-
-#include <mutex>
-
-#include "common.h"
+#include "blas.h"
 
 namespace moe {
 namespace {
-
-constexpr size_t kBlasWs = size_t{32} << 20;  // rocBLAS workspace slice (bytes)
 
 constexpr int VT = 256;  // threads per block of the row kernels (one token row per block)
 constexpr int VU = 4;    // float4 loads in flight per thread
@@ -167,62 +161,6 @@ __global__ __launch_bounds__(256) void voc_to_bf16_kernel(const float* __restric
   *reinterpret_cast<uint32_t*>(b + i) = pack_bf16x2(a[i], a[i + 1]);
 }
 
-// One rocBLAS handle per device, created on first use; the handle is not
-// reentrant, so each call's stream/workspace binding and GEMMs run under the
-// device's lock.
-constexpr int kMaxDev = 64;
-struct Blas {
-  std::mutex mu;
-  rocblas_handle h = nullptr;
-};
-Blas& blas_for(int dev) {
-  static Blas b[kMaxDev];
-  return b[dev];
-}
-
-hipError_t blas_status(rocblas_status st) {
-  return st == rocblas_status_success ? hipSuccess : hipErrorUnknown;
-}
-
-hipError_t blas_for_current(Blas** out) {
-  int dev = 0;
-  if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
-  if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
-  *out = &blas_for(dev);
-  return hipSuccess;
-}
-
-// With the device's lock held: create the handle on first use (atomics off,
-// so every product is summed in a fixed order and results repeat bit for
-// bit), then bind the call's stream and its slice of the caller's workspace.
-hipError_t blas_bind(Blas& B, hipStream_t s, void* ws) {
-  if (B.h == nullptr) {
-    rocblas_handle h = nullptr;
-    if (hipError_t e = blas_status(rocblas_create_handle(&h)); e != hipSuccess) return e;
-    if (hipError_t e = blas_status(rocblas_set_atomics_mode(h, rocblas_atomics_not_allowed));
-        e != hipSuccess) {
-      rocblas_destroy_handle(h);
-      return e;
-    }
-    B.h = h;
-  }
-  if (hipError_t e = blas_status(rocblas_set_stream(B.h, s)); e != hipSuccess) return e;
-  return blas_status(rocblas_set_workspace(B.h, ws, kBlasWs));
-}
-
-// C (fp32 or bf16, column-major m x n, ldc) = alpha op(A) op(B) + beta C with
-// bf16 A, B and fp32 accumulation
-rocblas_status gemm(rocblas_handle h, bool ta, bool tb, int m, int n, int k, const void* A,
-                    int lda, const void* B, int ldb, float beta, void* C, bool c_bf16, int ldc) {
-  const float alpha = 1.0f;
-  const rocblas_datatype ct = c_bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
-  return rocblas_gemm_ex(h, ta ? rocblas_operation_transpose : rocblas_operation_none,
-                         tb ? rocblas_operation_transpose : rocblas_operation_none, m, n, k,
-                         &alpha, A, rocblas_datatype_bf16_r, lda, B, rocblas_datatype_bf16_r, ldb,
-                         &beta, C, ct, ldc, C, ct, ldc, rocblas_datatype_f32_r,
-                         rocblas_gemm_algo_standard, 0, 0);
-}
-
 }  // namespace
 
 size_t vocab_fwd_ws_bytes(int64_t N, int64_t vblock) {
@@ -255,17 +193,15 @@ hipError_t launch_vocab_fwd(const uint16_t* x, const uint16_t* w, const int32_t*
   float* yt = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * static_cast<size_t>(N), 256);
   void* bws = p;
-  Blas* B = nullptr;
-  if (hipError_t e = blas_for_current(&B); e != hipSuccess) return e;
-  std::lock_guard<std::mutex> g(B->mu);
-  if (hipError_t e = blas_bind(*B, s, bws); e != hipSuccess) return e;
+  BlasLease B(s, bws);
+  if (hipError_t e = B.status(); e != hipSuccess) return e;
   const unsigned gr = static_cast<unsigned>(N);
   for (int64_t b0 = 0; b0 < V; b0 += vblock) {
     const int vb = static_cast<int>(std::min<int64_t>(vblock, V - b0));
     const int pitch = static_cast<int>(align_up(vb, 8));
     // Y[N][vb] = X[N][H] W[H][b0 : b0 + vb]
-    if (hipError_t e = blas_status(gemm(B->h, false, false, vb, static_cast<int>(N), H, w + b0,
-                                        static_cast<int>(V), x, H, 0.0f, Y, false, pitch));
+    if (hipError_t e = gemm_bf16(B.handle(), false, false, vb, static_cast<int>(N), H, w + b0,
+                                 static_cast<int>(V), 0, x, H, 0, 0.0f, Y, false, pitch, 0);
         e != hipSuccess)
       return e;
     prof_begin(K_VOC_LSE, s);
@@ -294,10 +230,8 @@ hipError_t launch_vocab_bwd(const uint16_t* x, const uint16_t* w, const int32_t*
   float* dxa = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * static_cast<size_t>(N) * H, 256);
   void* bws = p;
-  Blas* B = nullptr;
-  if (hipError_t e = blas_for_current(&B); e != hipSuccess) return e;
-  std::lock_guard<std::mutex> g(B->mu);
-  if (hipError_t e = blas_bind(*B, s, bws); e != hipSuccess) return e;
+  BlasLease B(s, bws);
+  if (hipError_t e = B.status(); e != hipSuccess) return e;
   const int64_t nx = N * H;
   voc_fill_kernel<<<static_cast<unsigned>(ceil_div(nx, 256)), 256, 0, s>>>(dxa, nx);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
@@ -306,8 +240,8 @@ hipError_t launch_vocab_bwd(const uint16_t* x, const uint16_t* w, const int32_t*
     const int vb = static_cast<int>(std::min<int64_t>(vblock, V - b0));
     const int pitch = static_cast<int>(align_up(vb, 8));
     // Y[N][vb] = X W[:, b0 : b0 + vb]   (recomputed)
-    if (hipError_t e = blas_status(gemm(B->h, false, false, vb, n, H, w + b0, ldw, x, H, 0.0f, Y,
-                                        false, pitch));
+    if (hipError_t e = gemm_bf16(B.handle(), false, false, vb, n, H, w + b0, ldw, 0, x, H, 0, 0.0f,
+                                 Y, false, pitch, 0);
         e != hipSuccess)
       return e;
     prof_begin(K_VOC_GRAD, s);
@@ -316,13 +250,13 @@ hipError_t launch_vocab_bwd(const uint16_t* x, const uint16_t* w, const int32_t*
     prof_end(K_VOC_GRAD, s);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     // dX[N][H] += G[N][vb] W[:, b0 : b0 + vb]^T
-    if (hipError_t e = blas_status(gemm(B->h, true, false, H, n, vb, w + b0, ldw, G, pitch, 1.0f,
-                                        dxa, false, H));
+    if (hipError_t e = gemm_bf16(B.handle(), true, false, H, n, vb, w + b0, ldw, 0, G, pitch, 0,
+                                 1.0f, dxa, false, H, 0);
         e != hipSuccess)
       return e;
     // dW[:, b0 : b0 + vb] = X^T G
-    if (hipError_t e = blas_status(gemm(B->h, false, true, vb, H, n, G, pitch, x, H, 0.0f, dw + b0,
-                                        true, ldw));
+    if (hipError_t e = gemm_bf16(B.handle(), false, true, vb, H, n, G, pitch, 0, x, H, 0, 0.0f,
+                                 dw + b0, true, ldw, 0);
         e != hipSuccess)
       return e;
   }

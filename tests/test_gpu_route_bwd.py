@@ -8,8 +8,10 @@ bias gradient and dlogits W_r^T in fp64.
 
 Tolerances: dlogits differ only by the fp32 exponential and rounding
 (1e-5 of the largest value); dW_r and dbias are fp32 sums over T tokens
-(relative rounding below T * 2^-24, and well below 1e-3 for these T);
-dx is rounded to bf16 (2^-9 relative), checked at the layer-wide 1e-2.
+(relative rounding below T * 2^-24, and well below 1e-3 for these T; the
+matrix-core path for large T*d*E adds the 2^-17 relative error of its bf16
+hi/lo parts); dx is rounded to bf16 (2^-9 relative), checked at the
+layer-wide 1e-2.
 """
 import sys
 
@@ -71,6 +73,10 @@ SMALL = [
     ("E1024", 40, 16, 1024, 16, 1, False, True, True, True),
     ("t1", 1, 24, 5, 2, 0, False, True, True, True),
     ("no_dx", 257, 8, 3, 2, 0, False, True, True, True),
+    # T*d*E >= 2^28: the matrix-core path (bf16 hi/lo parts), with a
+    # shorter last token chunk and d not a multiple of 256 in the second
+    ("mfma", 2048, 1024, 128, 6, 0, True, True, True, True),
+    ("mfma_ragged", 2100, 1032, 128, 4, 1, False, False, True, False),
 ]
 
 
@@ -106,6 +112,12 @@ def test_route_bwd_small(case):
             mask = np.ones((T, E), bool)
             np.put_along_axis(mask, idx_h.astype(np.int64), False, axis=1)
             assert np.all(P.f64(dl)[mask] == 0.0)
+    if name.startswith("mfma"):  # the matrix-core path repeats every bit too
+        again = _run_bwd(x, w, lg, idx, gate, dgate, renorm, dx_in, acc, with_db, want_dl)
+        for ta, tb in zip((dw, db, dx), again[:3]):
+            if ta is not None:
+                v = torch.int16 if ta.dtype == torch.bfloat16 else torch.int32
+                assert torch.equal(ta.view(v), tb.view(v))
     _say(f"[route_bwd] {name} ok {errs}")
 
 
