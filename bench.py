@@ -8,7 +8,12 @@ timed region starts.  A second timed loop adds the router backward (dW_r,
 dbias and the router's share of dx) to every step: "with_router_backward".
 
 Prints ONE JSON line (rank 0).  Default workload: T=4096 tokens, d=2048,
-E=64 experts, top-6, f=1408 SwiGLU (bf16, fp32 router, seed 0).
+E=64 experts, top-6, f=1408 SwiGLU (bf16, fp32 router, seed 0).  Besides the
+step it reports, each under its own key: per-kernel times and roofline
+fractions, the memory-efficient (chunked) forward, the vendor batched GEMM
+on the same six products (context), least-loaded expert parallelism on the
+skewed workload's routing, the blockwise vocabulary loss, and the CPU
+oracle's rate on a bounded sample.
 """
 from __future__ import annotations
 

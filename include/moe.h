@@ -15,8 +15,9 @@
  *  - bf16 values are raw IEEE bfloat16 bit patterns (moe_bf16); fp32->bf16 is
  *    round-to-nearest-even.  All arrays are dense and row-major.
  *  - Every pointer is DEVICE memory owned by the caller; the library
- *    allocates nothing (save the vocabulary loss's rocBLAS handle) and
- *    keeps no reference after the call returns.
+ *    allocates nothing (save one rocBLAS handle per device, created by the
+ *    first call that needs it: the vocabulary loss, or a router backward
+ *    with T*d*E >= 2^28) and keeps no reference after the call returns.
  *    Required pointers must be non-NULL and 16-byte aligned.
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *    Calls only enqueue work and return; no call synchronises the device.
@@ -100,11 +101,16 @@ int moe_route(const moe_bf16* x, const float* w_router, const float* router_bias
  *               dgate[t][i] gate[t][i], p = softmax of logits[t] over all E;
  *   renorm = 1: dlogits[t][topk_idx[t][i]] = gate[t][i] (dgate[t][i] - s),
  *               0 for experts not chosen.
- * Then, all in fp32 with fixed summation orders (bitwise reproducible):
+ * Then, with fixed summation orders (bitwise reproducible):
  *   dw_router[j][e] = sum over t of float(x[t][j]) dlogits[t][e]   (overwritten)
  *   dbias[e]        = sum over t of dlogits[t][e]                  (optional)
- *   dx[t][j]        = bf16( [float(dx[t][j]) +] sum over e ascending of
+ *   dx[t][j]        = bf16( [float(dx[t][j]) +] sum over e of
  *                     dlogits[t][e] w_router[j][e] )               (optional)
+ * in fp32 on the vector ALUs (e ascending for dx) when T*d*E < 2^28, and
+ * above that on the bf16 matrix cores with each fp32 operand v taken as
+ * bf16(v) + bf16(v - bf16(v)) (relative error <= 2^-17, fp32 accumulation,
+ * rocBLAS products with atomics off; token chunks of dw_router summed in
+ * order).  dlogits and dbias are fp32 in both.
  * dx_accumulate = 1 adds the router's share to the expert path's input
  * gradient already in dx (e.g. from the unit-weight moe_combine of dx_perm),
  * giving the whole layer's dx; dx is then read and written in place (the one
@@ -266,9 +272,10 @@ int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, const float*
  * multiple of 8, vblock a positive multiple of 8, N * vblock < 2^40.
  * workspace: moe_vocab_loss_workspace_bytes() bytes (serves both calls;
  * about 6 N vblock + 4 N H bytes + 32 MiB).  The three products per block
- * are rocBLAS GEMMs: the first call on a device creates that device's
- * rocBLAS handle (the one allocation the library makes; it is kept until
- * the process ends), and calls on one device serialise on its host lock.
+ * are rocBLAS GEMMs: the first call on a device that needs rocBLAS creates
+ * that device's handle (the one allocation the library makes; it is kept
+ * until the process ends), and calls that use it on one device serialise on
+ * its host lock.
  */
 int moe_vocab_loss_workspace_bytes(int64_t N, int H, int64_t V, int64_t vblock, size_t* bytes);
 int moe_vocab_loss_fwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* target, int64_t N,
