@@ -91,6 +91,8 @@ SMALL = {
     "renorm": W.Workload("renorm", T=256, d=128, E=8, k=3, f=64, renorm=1),
     "t1": W.Workload("t1", T=1, d=24, E=5, k=2, f=16),
     "min_dims": W.Workload("min_dims", T=70, d=8, E=3, k=2, f=8),
+    # the limits: MOE_MAX_E experts, MOE_MAX_K slots (most experts get 0-2 rows)
+    "max_E_k": W.Workload("max_E_k", T=96, d=64, E=1024, k=16, f=32),
 }
 
 
