@@ -780,20 +780,27 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   // the expert weights in the forward and data-gradient GEMMs.  The single
   // sync of step s (after its last fragment reads) waits for step s + 1, then
   // prepares F for step s + 2 and S for step s + 3, into the slots step s has
-  // freed (an N-contiguous operand as two halves of 32 k).  Their 16 loads go
-  // out between the MFMAs of the next four sub-steps (the last of step s, the
-  // first three of step s + 1), never more than six per sub-step, F's first:
-  // the memory path takes them at an even rate instead of in one burst.
+  // freed (an N-contiguous operand as two halves of 32 k).  With both
+  // operands K-contiguous (the data gradients) their loads go out between the
+  // MFMAs of the next four sub-steps (the last of step s, the first three of
+  // step s + 1), never more than six per sub-step, F's first: the memory path
+  // takes them at an even rate instead of in one burst.  With an N-contiguous
+  // operand (forward and weight gradients) the loads go out in one burst
+  // right after the sync, F's first: its two-half issue state held across
+  // four sub-steps would not fit the scalar registers (the spills and the
+  // branches around each deferred load cost more than the burst does).
   constexpr bool A_K = !A_N, B_N = !B_K;
   constexpr bool A_FIRST = !WGRAD;  // F = A (activations), S = B (weights)
   constexpr int NA = A_FIRST ? 2 : 3, NB = NRING - NA;
   constexpr int LA = A_K ? LOADS_K : 2 * LOADS_H;  // loads per wave of one step's issue
   constexpr int LB = B_K ? LOADS_K : 2 * LOADS_H;
-  // Load schedule over the four sub-steps that follow a sync (see mma_mix):
+  // Spread schedule over the four sub-steps that follow a sync (see mma_mix):
   // issue order F0, F1, S0, F2, F3, S1, S2, S3.  At the sync of step s the
   // loads issued after the last of F(s + 1) (the later of the two it needs)
-  // are S(s + 3)'s loads 1..3: the vector-memory count it may leave.
-  constexpr int X_END = 3;
+  // are S(s + 3)'s loads 1..3: the vector-memory count it may leave.  In a
+  // burst (F0..F3, S0..S3) they are all four of S(s + 3)'s.
+  constexpr bool BURST = A_N || B_N;
+  constexpr int X_END = BURST ? 4 : 3;
   static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
   static_assert(LA == 4 && LB == 4 && NA + NB == NRING && (NA == 2 || NB == 2),
                 "the sync count assumes this ring");
@@ -1016,21 +1023,33 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       constexpr bool last = LAST;
       load_frags(nxt, s, 1);
       __builtin_amdgcn_sched_barrier(0);
-      mma_mix(cur, std::integral_constant<int, 1>{}, sb, sa, pend);
+      mma_mix(cur, std::integral_constant<int, 1>{}, sb, sa, !BURST && pend);
       __builtin_amdgcn_sched_barrier(0);
       load_frags(cur, s, 2);
       __builtin_amdgcn_sched_barrier(0);
-      mma_mix(nxt, std::integral_constant<int, 2>{}, sb, sa, pend);
+      mma_mix(nxt, std::integral_constant<int, 2>{}, sb, sa, !BURST && pend);
       __builtin_amdgcn_sched_barrier(0);
       load_frags(nxt, s, 3);
       __builtin_amdgcn_sched_barrier(0);
-      mma_mix(cur, std::integral_constant<int, 3>{}, sb, sa, pend);
+      mma_mix(cur, std::integral_constant<int, 3>{}, sb, sa, !BURST && pend);
       __builtin_amdgcn_sched_barrier(0);
       sync();
       wait_vmcnt<X_END>();
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (!last) {
+      if constexpr (!last && BURST) {
+        if constexpr (A_FIRST) {
+          issue_stepA();
+          issue_stepB();
+        } else {
+          issue_stepB();
+          issue_stepA();
+        }
+        lgkm_drained();
+        load_frags(cur, s + 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(nxt);
+      } else if constexpr (!last) {
         sb = prep_stepB();
         sa = prep_stepA();
         pend = true;
