@@ -774,13 +774,14 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   };
 
   // ------------------------------------------------------------ LDS rings
-  // NA slots of UNIT bytes for operand A, then NB for operand B, one K step
-  // per slot.  One operand (F, two slots) is loaded one step ahead, the
-  // other (S, three slots) two: S is the one whose tiles miss L2 more often,
-  // the expert weights in the forward and data-gradient GEMMs.  The single
-  // sync of step s (after its last fragment reads) waits for step s + 1, then
-  // prepares F for step s + 2 and S for step s + 3, into the slots step s has
-  // freed (an N-contiguous operand as two halves of 32 k).  With both
+  // NA = 2 slots of UNIT bytes for operand A, then NB = 3 for operand B, one
+  // K step per slot.  A (called F below) is loaded one step ahead, B (S) two:
+  // in the forward and data-gradient GEMMs B is the expert weights, whose
+  // tiles miss L2 more often; in the weight gradients B is dH (the reverse
+  // order measured 5 % slower there).  The single sync of step s (after its
+  // last fragment reads) waits for step s + 1, then prepares F for step s + 2
+  // and S for step s + 3, into the slots step s has freed (an N-contiguous
+  // operand as two halves of 32 k).  With both
   // operands K-contiguous (the data gradients) their loads go out between the
   // MFMAs of the next four sub-steps (the last of step s, the first three of
   // step s + 1), never more than six per sub-step, F's first: the memory path
@@ -790,8 +791,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   // four sub-steps would not fit the scalar registers (the spills and the
   // branches around each deferred load cost more than the burst does).
   constexpr bool A_K = !A_N, B_N = !B_K;
-  constexpr bool A_FIRST = !WGRAD;  // F = A (activations), S = B (weights)
-  constexpr int NA = A_FIRST ? 2 : 3, NB = NRING - NA;
+  constexpr int NA = 2, NB = NRING - NA;
   constexpr int LA = A_K ? LOADS_K : 2 * LOADS_H;  // loads per wave of one step's issue
   constexpr int LB = B_K ? LOADS_K : 2 * LOADS_H;
   // Spread schedule over the four sub-steps that follow a sync (see mma_mix):
@@ -802,7 +802,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   constexpr bool BURST = A_N || B_N;
   constexpr int X_END = BURST ? 4 : 3;
   static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
-  static_assert(LA == 4 && LB == 4 && NA + NB == NRING && (NA == 2 || NB == 2),
+  static_assert(LA == 4 && LB == 4 && NA == 2 && NB == 3,
                 "the sync count assumes this ring");
 
   lds_char* const ring = (lds_char*)(lds);  // address-space cast
@@ -839,9 +839,8 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   // run ahead across tile boundaries.  Past the end of the stream the load
   // iterators issue the same number of loads out of range (they write zeros
   // to slots nobody reads), which keeps every sync's count exact.  After a
-  // tile's last step its A slot (its high halves, when both operands are
-  // N-contiguous) holds the epilogue patches; the refill of that slot waits
-  // until the epilogue is done.
+  // tile's last step, B's slot of that step holds the epilogue patches; the
+  // refill of that slot waits until the epilogue is done.
   const Tables tb{g.mt_start, g.offsets, g.wk_start, g.nz_start};
   const i32x4 nil = make_rsrc(nullptr, 0);
   TileIter<MODE> itc, ita, itb;
@@ -980,7 +979,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
             // entry: F load (first operand) or S load, with its index
             constexpr bool is_f = g < 2 && j < 2;
             constexpr int q = is_f ? 2 * g + j : (g < 2 ? g : g);
-            constexpr bool is_a = is_f == A_FIRST;
+            constexpr bool is_a = is_f;
             if (pend) {
               if constexpr (is_a) emitA(sa, q);
               else emitB(sb, q);
@@ -994,13 +993,8 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     // (F before S)
     static_for<3>([&](auto V) {
       constexpr int v = static_cast<int>(V) - 3;
-      if constexpr (A_FIRST) {
-        if constexpr (v + NA >= 0) issue_stepA();
-        if constexpr (v + NB >= 0) issue_stepB();
-      } else {
-        if constexpr (v + NB >= 0) issue_stepB();
-        if constexpr (v + NA >= 0) issue_stepA();
-      }
+      if constexpr (v + NA >= 0) issue_stepA();
+      if constexpr (v + NB >= 0) issue_stepB();
     });
     wait_vmcnt<X_END>();
     lgkm_drained();
@@ -1038,13 +1032,8 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (!last && BURST) {
-        if constexpr (A_FIRST) {
-          issue_stepA();
-          issue_stepB();
-        } else {
-          issue_stepB();
-          issue_stepA();
-        }
+        issue_stepA();
+        issue_stepB();
         lgkm_drained();
         load_frags(cur, s + 1, 0);
         __builtin_amdgcn_sched_barrier(0);
@@ -1059,8 +1048,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         mma_mix(nxt, std::integral_constant<int, 0>{}, sb, sa, true);
       } else {
         // F goes out now; S's refill would land in the epilogue patches
-        if constexpr (A_FIRST) issue_stepA();
-        else issue_stepB();
+        issue_stepA();
         pend = false;
         __builtin_amdgcn_sched_barrier(0);
         mma(nxt);
@@ -1071,10 +1059,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     while (true) {
       for (int kk = 0; kk + 1 < tc.nk; ++kk) step(std::false_type{});
       step(std::true_type{});
-      // epilogue patches: S's slot of the tile's last step
+      // epilogue patches: S's (B's) slot of the tile's last step
       const int ls = s - 1;
-      lds_char* const patch =
-          ring + (A_FIRST ? (NA + ls % NB) : (ls % NA)) * UNIT + w * PATCH_BYTES;
+      lds_char* const patch = ring + (NA + ls % NB) * UNIT + w * PATCH_BYTES;
       epilogue(tc, patch);
       zero_acc();
       // the patch reads are done once the LDS counter drains; the stores stay
@@ -1084,8 +1071,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       __builtin_amdgcn_sched_barrier(0);
       tc = itc.next(g, tb);
       if (!tc.valid) break;
-      if constexpr (A_FIRST) issue_stepB();  // S's deferred refill
-      else issue_stepA();
+      issue_stepB();  // S's deferred refill
       lgkm_drained();
       load_frags(cur, s, 0);
     }
