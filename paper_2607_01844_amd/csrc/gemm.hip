@@ -215,12 +215,24 @@ struct KOperand {
 // sub-tiles of 128 (sub-tile j starts at ptr_j, has cols_j valid columns and
 // range_j readable bytes); k < kmax valid.  Loads move half a step (32 k)
 // at a time, so that the half consumed first is refilled half a step
-// earlier.  The descriptor base advances with k, so lane offsets stay below
-// 32 rows.  LDS per half: two sub-tiles [32 k][128 cols] bf16, 256-byte
+// earlier.  The descriptor base advances with k (two scalar adds per
+// sub-tile and half), so lane offsets stay below 32 rows; every lane's row
+// and column are checked against krem and cols_j, so the descriptor range,
+// fixed at the tile's start, is only a bound that valid lanes never reach.  LDS per half: two sub-tiles [32 k][128 cols] bf16, 256-byte
 // rows, 16-byte chunk c of row k at ((c ^ (4 (k & 3))) << 4): the 32 lanes of
 // one ds_read_b64_tr_b16 pass (4 rows x 4 chunks x 2 halves) hit all 64 banks.
 __device__ __forceinline__ int noff(int k, int col) {
   return k * 256 + ((((col >> 3) ^ (4 * (k & 3)))) << 4) + ((col >> 2) & 1) * 8;
+}
+
+// base address (words 0-1 of a descriptor without stride) + bytes
+__device__ __forceinline__ i32x4 rsrc_advance(i32x4 r, uint32_t bytes) {
+  const uint64_t a =
+      ((static_cast<uint64_t>(static_cast<uint32_t>(r[1]) & 0xffffu) << 32) | static_cast<uint32_t>(r[0])) +
+      bytes;
+  r[0] = static_cast<int>(a & 0xffffffffu);
+  r[1] = static_cast<int>((a >> 32) & 0xffffu);
+  return r;
 }
 
 struct NOperand {
@@ -230,47 +242,45 @@ struct NOperand {
   uint32_t ld;
   int cols0, cols1;
   int kmax;
-
-  // Half h (0, 1) of step kt.  Load q (0..3) of this wave: I = 4 wave + q
-  // covers rows 4 (I % 8) .. +3 of sub-tile I / 8; lane l takes row
-  // k = 4 (I % 8) + l / 16 and column 8 ((l % 16) ^ (4 (k % 4))).
-  struct Issue {
-    i32x4 r0, r1;
-    uint32_t ld, lds, vb;
-    int col, cols0, cols1, krem, kl;
-    __device__ __forceinline__ void emit(int q, int wave) const {
-      const int I = wave * LOADS_H + q;
-      const int kr = (I & 7) * 4;
-      const bool ok = col < ((I >> 3) ? cols1 : cols0) && kl < krem - kr;
-      load_lds16((I >> 3) ? r1 : r0, ok ? vb + static_cast<uint32_t>(kr) * ld : OOB,
-                 lds + (I >> 3) * (HALF / 2) + (I & 7) * 1024);
-    }
-  };
-  __device__ __forceinline__ Issue prep(int kt, int h, uint32_t lds_half, int lane_in) const {
-    const int k0 = kt * BK + h * (BK / 2);
-    const int64_t adv = static_cast<int64_t>(k0) * ld;
-    Issue p;
-    p.r0 = make_rsrc(reinterpret_cast<const char*>(ptr0) + adv, range0 - adv);
-    p.r1 = make_rsrc(reinterpret_cast<const char*>(ptr1) + adv, range1 - adv);
-    const int lane = opaque(lane_in);
-    p.kl = lane >> 4;                                // row within the load's 4 rows
-    p.col = ((lane & 15) ^ (4 * p.kl)) * 8;          // (row % 4 == kl)
-    p.vb = static_cast<uint32_t>(p.kl) * ld + static_cast<uint32_t>(p.col) * 2u;
-    p.ld = ld;
-    p.cols0 = cols0;
-    p.cols1 = cols1;
-    p.krem = kmax - k0;
-    p.lds = lds_half;
-    return p;
+  // load stream: descriptors of the next half's first row, valid k from there
+  i32x4 rn0, rn1;
+  int krem;
+  __device__ __forceinline__ void start() {
+    rn0 = make_rsrc(ptr0, range0);
+    rn1 = make_rsrc(ptr1, range1);
+    krem = kmax;
   }
-  static __device__ __forceinline__ Issue none(const i32x4& nil, uint32_t lds_half) {
-    Issue p;
-    p.r0 = p.r1 = nil;
-    p.ld = p.vb = 0;
-    p.col = p.kl = p.krem = 0;
-    p.cols0 = p.cols1 = 0;
-    p.lds = lds_half;
-    return p;
+
+  // This wave's loads of the next half (halves are issued in order from
+  // start()).  Load q (0 .. LOADS_H - 1), I = LOADS_H wave + q, covers rows
+  // 4 (I % 8) .. +3 of sub-tile I / 8 (the same for all of a wave's loads);
+  // lane l takes row k = 4 (I % 8) + l / 16 and column 8 ((l % 16) ^ (4 (k % 4))).
+  __device__ __forceinline__ void issue(uint32_t lds_half, int lane_in, int wave) {
+    static_assert(8 % LOADS_H == 0, "a wave's loads stay in one sub-tile");
+    const int lane = opaque(lane_in);
+    const int kl = lane >> 4;                        // row within the load's 4 rows
+    const int col = ((lane & 15) ^ (4 * kl)) * 8;    // (row % 4 == kl)
+    const uint32_t vb = static_cast<uint32_t>(kl) * ld + static_cast<uint32_t>(col) * 2u;
+    const int sub = (wave * LOADS_H) >> 3;
+    const i32x4 rs = sub ? rn1 : rn0;
+    const int cols = sub ? cols1 : cols0;
+    static_for<LOADS_H>([&](auto Q) {
+      const int I = wave * LOADS_H + Q;
+      const int kr = (I & 7) * 4;
+      const bool ok = col < cols && kl < krem - kr;
+      load_lds16(rs, ok ? vb + static_cast<uint32_t>(kr) * ld : OOB,
+                 lds_half + sub * (HALF / 2) + (I & 7) * 1024);
+    });
+    rn0 = rsrc_advance(rn0, (BK / 2) * ld);
+    rn1 = rsrc_advance(rn1, (BK / 2) * ld);
+    krem -= BK / 2;
+  }
+  // the same number of loads, all out of range (zeros into an unused slot)
+  static __device__ __forceinline__ void issue_none(const i32x4& nil, uint32_t lds_half, int wave) {
+    static_for<LOADS_H>([&](auto Q) {
+      const int I = wave * LOADS_H + Q;
+      load_lds16(nil, OOB, lds_half + (I >> 3) * (HALF / 2) + (I & 7) * 1024);
+    });
   }
   // MFMA fragment of tile column block c0 (multiple of 32) from one half:
   // lane l gets 8 consecutive k (k-group l/32 of substep s, 0..1, of the
@@ -855,111 +865,111 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     BOp B;
     bool hava = false, havb = false;
     int kta = 0, ktb = 0, ga = 0, gb = 0;  // step within the load tile; stream step
-    using AIssue = typename AOp::Issue;
-    using BIssue = typename BOp::Issue;
-    // h = -1: a K-contiguous unit; 0 / 1: low / high half of an N-contiguous
-    // step.  prep advances the operand's load stream by one issue and returns
-    // the issue's loads, which the caller emits (at once or between MFMAs).
-    auto prepA = [&](int h) __attribute__((always_inline)) {
+    // Each operand's load stream advances one issue at a time: a K-contiguous
+    // unit (h = -1) or the low / high half (h = 0 / 1) of an N-contiguous
+    // step.  `next_issue` moves the stream to that issue's tile and returns
+    // the LDS address it fills (-1: past the end of the stream).
+    auto next_issueA = [&](int h) __attribute__((always_inline)) {
       if (h <= 0 && tla.valid && kta >= tla.nk) {
         tla = ita.next(g, tb);
         kta = 0;
         hava = false;
       }
-      const uint32_t base = lds0 + (ga % NA) * UNIT + (h > 0 ? HALF : 0);
-      AIssue p;
-      if (tla.valid) {
-        if (!hava) {
-          setupA(tla, A);
-          hava = true;
-        }
-        if constexpr (A_N) p = A.prep(kta, h, base, lane);
-        else p = A.prep(kta, base, lane);
-      } else {
-        p = AOp::none(nil, base);
+      if (tla.valid && !hava) {
+        setupA(tla, A);
+        if constexpr (A_N) A.start();
+        hava = true;
       }
-      if (h != 0) {
-        ++kta;
-        ++ga;
-      }
-      return p;
+      return lds0 + (ga % NA) * UNIT + (h > 0 ? HALF : 0);
     };
-    auto prepB = [&](int h) __attribute__((always_inline)) {
+    auto next_issueB = [&](int h) __attribute__((always_inline)) {
       if (h <= 0 && tlb.valid && ktb >= tlb.nk) {
         tlb = itb.next(g, tb);
         ktb = 0;
         havb = false;
       }
-      const uint32_t base = lds0 + (NA + gb % NB) * UNIT + (h > 0 ? HALF : 0);
-      BIssue p;
-      if (tlb.valid) {
-        if (!havb) {
-          setupB(tlb, B);
-          havb = true;
-        }
-        if constexpr (B_N) p = B.prep(ktb, h, base, lane);
-        else p = B.prep(ktb, base, lane);
-      } else {
-        p = BOp::none(nil, base);
+      if (tlb.valid && !havb) {
+        setupB(tlb, B);
+        if constexpr (B_N) B.start();
+        havb = true;
       }
+      return lds0 + (NA + gb % NB) * UNIT + (h > 0 ? HALF : 0);
+    };
+    auto done_issueA = [&](int h) __attribute__((always_inline)) {
+      if (h != 0) {
+        ++kta;
+        ++ga;
+      }
+    };
+    auto done_issueB = [&](int h) __attribute__((always_inline)) {
       if (h != 0) {
         ++ktb;
         ++gb;
       }
-      return p;
     };
-    // one step's loads of an operand: a K-contiguous unit, or the two halves
-    // of an N-contiguous step
+    // K-contiguous operands: prep returns the issue's loads, which the caller
+    // emits at once or between MFMAs (the spread schedule).
+    struct NoIssue {};
+    using AIssue = typename std::conditional<A_N, NoIssue, KOperand::Issue>::type;
+    using BIssue = typename std::conditional<B_N, NoIssue, KOperand::Issue>::type;
     struct StepA {
-      AIssue p0, p1;
+      AIssue p0;
     };
     struct StepB {
-      BIssue p0, p1;
+      BIssue p0;
     };
     auto prep_stepA = [&]() __attribute__((always_inline)) {
       StepA st;
-      if constexpr (A_N) {
-        st.p0 = prepA(0);
-        st.p1 = prepA(1);
-      } else {
-        st.p0 = prepA(-1);
+      if constexpr (A_K) {
+        const uint32_t base = next_issueA(-1);
+        st.p0 = tla.valid ? A.prep(kta, base, lane) : KOperand::none(nil, base);
+        done_issueA(-1);
       }
       return st;
     };
     auto prep_stepB = [&]() __attribute__((always_inline)) {
       StepB st;
-      if constexpr (B_N) {
-        st.p0 = prepB(0);
-        st.p1 = prepB(1);
-      } else {
-        st.p0 = prepB(-1);
+      if constexpr (B_K) {
+        const uint32_t base = next_issueB(-1);
+        st.p0 = tlb.valid ? B.prep(ktb, base, lane) : KOperand::none(nil, base);
+        done_issueB(-1);
       }
       return st;
     };
-    // load q (0 .. LA - 1) of a step's issue
+    // load q (0 .. 3) of a K-contiguous step's issue
     auto emitA = [&](const StepA& st, int q) __attribute__((always_inline)) {
-      if constexpr (A_N) {
-        if (q < LOADS_H) st.p0.emit(q, w);
-        else st.p1.emit(q - LOADS_H, w);
-      } else {
-        st.p0.emit(q, w);
-      }
+      if constexpr (A_K) st.p0.emit(q, w);
     };
     auto emitB = [&](const StepB& st, int q) __attribute__((always_inline)) {
-      if constexpr (B_N) {
-        if (q < LOADS_H) st.p0.emit(q, w);
-        else st.p1.emit(q - LOADS_H, w);
+      if constexpr (B_K) st.p0.emit(q, w);
+    };
+    // one step's loads of an operand, at once (an N-contiguous operand as two
+    // halves, each issued straight from the operand's stream)
+    auto issue_stepA = [&]() __attribute__((always_inline)) {
+      if constexpr (A_N) {
+        static_for<2>([&](auto H) {
+          const uint32_t base = next_issueA(H);
+          if (tla.valid) A.issue(base, lane, w);
+          else NOperand::issue_none(nil, base, w);
+          done_issueA(H);
+        });
       } else {
-        st.p0.emit(q, w);
+        const StepA st = prep_stepA();
+        static_for<LA>([&](auto Q) { emitA(st, Q); });
       }
     };
-    auto issue_stepA = [&]() __attribute__((always_inline)) {
-      const StepA st = prep_stepA();
-      static_for<LA>([&](auto Q) { emitA(st, Q); });
-    };
     auto issue_stepB = [&]() __attribute__((always_inline)) {
-      const StepB st = prep_stepB();
-      static_for<LB>([&](auto Q) { emitB(st, Q); });
+      if constexpr (B_N) {
+        static_for<2>([&](auto H) {
+          const uint32_t base = next_issueB(H);
+          if (tlb.valid) B.issue(base, lane, w);
+          else NOperand::issue_none(nil, base, w);
+          done_issueB(H);
+        });
+      } else {
+        const StepB st = prep_stepB();
+        static_for<LB>([&](auto Q) { emitB(st, Q); });
+      }
     };
     // the 8 MFMAs of one sub-step with group G of the load schedule spread
     // between them (group 0: F0, F1, S0; 1: F2, F3, S1; 2: S2; 3: S3)
