@@ -943,33 +943,53 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     auto emitB = [&](const StepB& st, int q) __attribute__((always_inline)) {
       if constexpr (B_K) st.p0.emit(q, w);
     };
-    // one step's loads of an operand, at once (an N-contiguous operand as two
-    // halves, each issued straight from the operand's stream)
-    auto issue_stepA = [&]() __attribute__((always_inline)) {
+    // Part p (0, 1) of a step's loads of an operand: an N-contiguous half,
+    // straight from the operand's stream; a K-contiguous unit is part 0.
+    auto issue_partA = [&](int p) __attribute__((always_inline)) {
       if constexpr (A_N) {
-        static_for<2>([&](auto H) {
-          const uint32_t base = next_issueA(H);
-          if (tla.valid) A.issue(base, lane, w);
-          else NOperand::issue_none(nil, base, w);
-          done_issueA(H);
-        });
-      } else {
+        const uint32_t base = next_issueA(p);
+        if (tla.valid) A.issue(base, lane, w);
+        else NOperand::issue_none(nil, base, w);
+        done_issueA(p);
+      } else if (p == 0) {
         const StepA st = prep_stepA();
         static_for<LA>([&](auto Q) { emitA(st, Q); });
       }
     };
-    auto issue_stepB = [&]() __attribute__((always_inline)) {
+    auto issue_partB = [&](int p) __attribute__((always_inline)) {
       if constexpr (B_N) {
-        static_for<2>([&](auto H) {
-          const uint32_t base = next_issueB(H);
-          if (tlb.valid) B.issue(base, lane, w);
-          else NOperand::issue_none(nil, base, w);
-          done_issueB(H);
-        });
-      } else {
+        const uint32_t base = next_issueB(p);
+        if (tlb.valid) B.issue(base, lane, w);
+        else NOperand::issue_none(nil, base, w);
+        done_issueB(p);
+      } else if (p == 0) {
         const StepB st = prep_stepB();
         static_for<LB>([&](auto Q) { emitB(st, Q); });
       }
+    };
+    auto issue_stepA = [&]() __attribute__((always_inline)) {
+      issue_partA(0);
+      issue_partA(1);
+    };
+    auto issue_stepB = [&]() __attribute__((always_inline)) {
+      issue_partB(0);
+      issue_partB(1);
+    };
+    // Burst schedule: the 8 MFMAs that follow a sync with the step's loads
+    // between them (F's parts, then S's), so that the matrix cores have work
+    // while the loads are issued.
+    auto mma_issue = [&](const Frags& F) __attribute__((always_inline)) {
+      static_for<8>([&](auto T) {
+        constexpr int t = T;
+        acc[t / 2][t % 2] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (t % 2 == 1) {
+          if constexpr (t < 4) issue_partA(t / 2);
+          else issue_partB(t / 2 - 2);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
     };
     // the 8 MFMAs of one sub-step with group G of the load schedule spread
     // between them (group 0: F0, F1, S0; 1: F2, F3, S1; 2: S2; 3: S3)
@@ -1042,12 +1062,11 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (!last && BURST) {
-        issue_stepA();
-        issue_stepB();
         lgkm_drained();
         load_frags(cur, s + 1, 0);
         __builtin_amdgcn_sched_barrier(0);
-        mma(nxt);
+        mma_issue(nxt);
+        lgkm_drained();
       } else if constexpr (!last) {
         sb = prep_stepB();
         sa = prep_stepA();
