@@ -5,19 +5,20 @@
 //   * 512 threads = 8 waves (two per SIMD) in a 2 x 4 grid; the block
 //     computes a 256 x 256 tile of C^T (rows = output columns n, cols =
 //     output rows m) with v_mfma_f32_32x32x16_bf16, each wave 128 rows x 64
-//     columns, so each lane ends up holding four consecutive output columns
-//     and stores 8 bytes at a time.
+//     columns; the epilogue passes each wave's block through LDS so that
+//     every global store moves 16 bytes per lane.
 //   * Operands move global -> LDS with buffer_load_dwordx4 ... lds (no
-//     register staging).  The buffer descriptor's range check turns every
-//     tail (rows past an expert's segment, k past K, columns past N) into
-//     zeros, so there is no padding and no per-element branching.
+//     register staging).  Out-of-range lanes (rows past an expert's segment,
+//     k past K, columns past N) get an offset past the buffer descriptor's
+//     range and read zeros, so there is no padding and no per-element
+//     branching.
 //   * K steps of 64 through a ring of five 32 KiB LDS slots (all 160 KiB):
-//     two for the operand the tile streams fastest and three for the other,
-//     so loads run up to three steps ahead of the MFMAs, spread evenly over
-//     the sub-steps between barriers; one barrier per step, and the stream
-//     of K steps continues across tile boundaries.  A step of 64 k makes
-//     every row of a K-contiguous tile one full 128-byte line, which the
-//     memory path moves at twice the rate of 64-byte halves.
+//     two for operand A (loaded one step ahead) and three for operand B (two
+//     steps ahead); a sync's loads go out between the eight MFMAs that follow
+//     it; one barrier per step, and the stream of K steps continues across
+//     tile boundaries.  A step of 64 k makes every row of a K-contiguous
+//     tile one full 128-byte line, which the memory path moves at twice the
+//     rate of 64-byte halves.
 //   * Operands stored K-contiguous (activations in the forward pass and the
 //     data gradients, weights in the data gradients) sit in LDS as
 //     [256 rows][64 k] and feed the MFMA with ds_read_b128.  Operands stored
@@ -791,26 +792,19 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   // order measured 5 % slower there).  The single sync of step s (after its
   // last fragment reads) waits for step s + 1, then prepares F for step s + 2
   // and S for step s + 3, into the slots step s has freed (an N-contiguous
-  // operand as two halves of 32 k).  With both
-  // operands K-contiguous (the data gradients) their loads go out between the
-  // MFMAs of the next four sub-steps (the last of step s, the first three of
-  // step s + 1), never more than six per sub-step, F's first: the memory path
-  // takes them at an even rate instead of in one burst.  With an N-contiguous
-  // operand (forward and weight gradients) the loads go out in one burst
-  // right after the sync, F's first: its two-half issue state held across
-  // four sub-steps would not fit the scalar registers (the spills and the
-  // branches around each deferred load cost more than the burst does).
+  // operand as two halves of 32 k).  These loads go out between the eight
+  // MFMAs that follow the sync, F's first, so the matrix cores have work
+  // while they are issued and the issue state is never held across
+  // sub-steps (spreading them over the whole step, as an earlier version
+  // did, cost scalar-register spills and a branch per load).
   constexpr bool A_K = !A_N, B_N = !B_K;
   constexpr int NA = 2, NB = NRING - NA;
   constexpr int LA = A_K ? LOADS_K : 2 * LOADS_H;  // loads per wave of one step's issue
   constexpr int LB = B_K ? LOADS_K : 2 * LOADS_H;
-  // Spread schedule over the four sub-steps that follow a sync (see mma_mix):
-  // issue order F0, F1, S0, F2, F3, S1, S2, S3.  At the sync of step s the
-  // loads issued after the last of F(s + 1) (the later of the two it needs)
-  // are S(s + 3)'s loads 1..3: the vector-memory count it may leave.  In a
-  // burst (F0..F3, S0..S3) they are all four of S(s + 3)'s.
-  constexpr bool BURST = A_N || B_N;
-  constexpr int X_END = BURST ? 4 : 3;
+  // At the sync of step s the loads issued after the last of F(s + 1) (the
+  // later of the two operands it needs) are S(s + 2)'s four: the
+  // vector-memory count it may leave.
+  constexpr int X_END = 4;
   static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
   static_assert(LA == 4 && LB == 4 && NA == 2 && NB == 3,
                 "the sync count assumes this ring");
@@ -908,7 +902,7 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       }
     };
     // K-contiguous operands: prep returns the issue's loads, which the caller
-    // emits at once or between MFMAs (the spread schedule).
+    // emits.
     struct NoIssue {};
     using AIssue = typename std::conditional<A_N, NoIssue, KOperand::Issue>::type;
     using BIssue = typename std::conditional<B_N, NoIssue, KOperand::Issue>::type;
@@ -975,9 +969,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       issue_partB(0);
       issue_partB(1);
     };
-    // Burst schedule: the 8 MFMAs that follow a sync with the step's loads
-    // between them (F's parts, then S's), so that the matrix cores have work
-    // while the loads are issued.
+    // The 8 MFMAs that follow a sync with the step's loads between them (F's
+    // parts, then S's), so that the matrix cores have work while the loads
+    // are issued.
     auto mma_issue = [&](const Frags& F) __attribute__((always_inline)) {
       static_for<8>([&](auto T) {
         constexpr int t = T;
@@ -991,32 +985,13 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         }
       });
     };
-    // the 8 MFMAs of one sub-step with group G of the load schedule spread
-    // between them (group 0: F0, F1, S0; 1: F2, F3, S1; 2: S2; 3: S3)
-    auto mma_mix = [&](const Frags& F, auto G, const StepB& sb, const StepA& sa, bool pend)
-        __attribute__((always_inline)) {
-      static_assert(LA == 4 && LB == 4, "load schedule");
-      constexpr int g = G;
-      constexpr int n = g < 2 ? 3 : 1;
+    // the 8 MFMAs of one sub-step, kept in this order
+    auto mma_seq = [&](const Frags& F) __attribute__((always_inline)) {
       static_for<8>([&](auto T) {
         constexpr int t = T;
         acc[t / 2][t % 2] =
             __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        static_for<n>([&](auto J) {
-          constexpr int j = J;
-          if constexpr ((j * 8) / n == t) {
-            // entry: F load (first operand) or S load, with its index
-            constexpr bool is_f = g < 2 && j < 2;
-            constexpr int q = is_f ? 2 * g + j : (g < 2 ? g : g);
-            constexpr bool is_a = is_f;
-            if (pend) {
-              if constexpr (is_a) emitA(sa, q);
-              else emitB(sb, q);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        });
       });
     };
     // prologue: the issues the syncs of steps -3, -2, -1 would have made
@@ -1038,47 +1013,34 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
     };
     // one K step; `last`: last step of the tile (its sync defers the refill of
-    // the patch slot).  sb / sa: the issue prepared at the previous sync,
-    // pend: whether its loads are still to go out (groups 1-3).
-    StepB sb{};
-    StepA sa{};
-    bool pend = false;
+    // the patch slot)
     auto step = [&](auto LAST) __attribute__((always_inline)) {
       constexpr bool last = LAST;
       load_frags(nxt, s, 1);
       __builtin_amdgcn_sched_barrier(0);
-      mma_mix(cur, std::integral_constant<int, 1>{}, sb, sa, !BURST && pend);
+      mma_seq(cur);
       __builtin_amdgcn_sched_barrier(0);
       load_frags(cur, s, 2);
       __builtin_amdgcn_sched_barrier(0);
-      mma_mix(nxt, std::integral_constant<int, 2>{}, sb, sa, !BURST && pend);
+      mma_seq(nxt);
       __builtin_amdgcn_sched_barrier(0);
       load_frags(nxt, s, 3);
       __builtin_amdgcn_sched_barrier(0);
-      mma_mix(cur, std::integral_constant<int, 3>{}, sb, sa, !BURST && pend);
+      mma_seq(cur);
       __builtin_amdgcn_sched_barrier(0);
       sync();
       wait_vmcnt<X_END>();
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (!last && BURST) {
+      if constexpr (!last) {
         lgkm_drained();
         load_frags(cur, s + 1, 0);
         __builtin_amdgcn_sched_barrier(0);
         mma_issue(nxt);
         lgkm_drained();
-      } else if constexpr (!last) {
-        sb = prep_stepB();
-        sa = prep_stepA();
-        pend = true;
-        lgkm_drained();
-        load_frags(cur, s + 1, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_mix(nxt, std::integral_constant<int, 0>{}, sb, sa, true);
       } else {
         // F goes out now; S's refill would land in the epilogue patches
         issue_stepA();
-        pend = false;
         __builtin_amdgcn_sched_barrier(0);
         mma(nxt);
       }
