@@ -156,11 +156,11 @@ struct KOperand {
   int kmax0, kmax1; // valid k of source 0 / 1
   int nk0;          // steps of source 0
 
-  // Load q (0..7) of this wave, I = 8 wave + q, fills tile rows 8 I .. 8 I + 7:
-  // lane l takes row r = 8 I + l / 8 and 16-byte chunk lc = (l % 8) ^ ((r / 2) % 8),
-  // where (r / 2) % 8 = 4 (q % 2) + l / 16.  prep() computes what the eight
-  // loads of one step share; Issue::emit(q) sends load q, so that the loads
-  // can be spread between MFMAs.
+  // Load q (0 .. LOADS_K - 1) of this wave, I = LOADS_K wave + q, fills tile
+  // rows 8 I .. 8 I + 7: lane l takes row r = 8 I + l / 8 and 16-byte chunk
+  // lc = (l % 8) ^ ((r / 2) % 8), where (r / 2) % 8 = 4 (q % 2) + l / 16.
+  // prep() computes what the loads of one step share; Issue::emit(q) sends
+  // load q.
   struct Issue {
     i32x4 rs;
     uint32_t ld, lds;     // row pitch; LDS base of the unit
@@ -795,8 +795,8 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   // operand as two halves of 32 k).  These loads go out between the eight
   // MFMAs that follow the sync, F's first, so the matrix cores have work
   // while they are issued and the issue state is never held across
-  // sub-steps (spreading them over the whole step, as an earlier version
-  // did, cost scalar-register spills and a branch per load).
+  // sub-steps (holding it across the whole step costs scalar-register
+  // spills and a branch per load).
   constexpr bool A_K = !A_N, B_N = !B_K;
   constexpr int NA = 2, NB = NRING - NA;
   constexpr int LA = A_K ? LOADS_K : 2 * LOADS_H;  // loads per wave of one step's issue
