@@ -33,7 +33,9 @@
  *  - cap >= T * min(k, num_local) is the row capacity of permuted buffers;
  *    rows [M, cap) of them are never read and are left unspecified.
  *  - Limits: 1 <= k <= MOE_MAX_K, k <= E <= MOE_MAX_E, T >= 0,
- *    T * k < 2^31, d and f multiples of 8 and >= 8.
+ *    T * k < 2^31, d, f and H multiples of 8 in [8, MOE_MAX_DIM] (the
+ *    kernels address a tile's rows with 32-bit offsets).  Calls outside the
+ *    limits return MOE_ERR_INVALID_ARG.
  *  - Device-side garbage (an expert id outside [0, E) in a caller-supplied
  *    topk_idx) is undefined behaviour.
  */
@@ -50,6 +52,7 @@ extern "C" {
 #define MOE_ABI_VERSION 1
 #define MOE_MAX_K 16
 #define MOE_MAX_E 1024
+#define MOE_MAX_DIM 262144
 #define MOE_LLEP_MAX_RANKS 64
 
 typedef uint16_t moe_bf16;

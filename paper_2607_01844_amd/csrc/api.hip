@@ -52,8 +52,8 @@ int check_tk(const char* fn, int64_t T, int E, int k) {
   return MOE_OK;
 }
 int check_dim(const char* fn, int v, const char* name) {
-  if (v < 8 || (v % 8) != 0) {
-    std::string m = std::string(name) + " must be a positive multiple of 8";
+  if (v < 8 || (v % 8) != 0 || v > MOE_MAX_DIM) {
+    std::string m = std::string(name) + " must be a multiple of 8 in [8, MOE_MAX_DIM]";
     return fail(MOE_ERR_INVALID_ARG, fn, m.c_str());
   }
   return MOE_OK;

@@ -21,6 +21,7 @@ MOE_BWD_DGRAD = 1
 MOE_BWD_WGRAD = 2
 MOE_MAX_K = 16
 MOE_MAX_E = 1024
+MOE_MAX_DIM = 262144
 
 C_SYMBOLS = (
     "moe_abi_version", "moe_status_string", "moe_last_error",

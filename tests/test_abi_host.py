@@ -81,6 +81,9 @@ Z = None
     ("k > MAX_K", lambda L: L.moe_route(P, P, Z, 10, 64, 64, 17, 0, P, P, P, Z, 0, Z)),
     ("E > MAX_E", lambda L: L.moe_route(P, P, Z, 10, 64, 2000, 2, 0, P, P, P, Z, 0, Z)),
     ("d % 8", lambda L: L.moe_route(P, P, Z, 10, 60, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("d > MAX_DIM", lambda L: L.moe_route(P, P, Z, 10, 262152, 8, 2, 0, P, P, P, Z, 0, Z)),
+    ("f > MAX_DIM", lambda L: L.moe_grouped_swiglu_fwd(P, P, 4, 100, 8, 262152, P, P, P, P, P,
+                                                       P, P, 1 << 20, Z)),
     ("renorm", lambda L: L.moe_route(P, P, Z, 10, 64, 8, 2, 2, P, P, P, Z, 0, Z)),
     ("null x", lambda L: L.moe_route(Z, P, Z, 10, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
     ("misaligned", lambda L: L.moe_route(MIS, P, Z, 10, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
