@@ -41,8 +41,10 @@ __device__ __forceinline__ void wait_vm() {
 // the row-major [d][E] array) and the block's token rows for those indices.
 // Per batch of 8 indices a lane reads its TE weights and, with one broadcast
 // 16-byte read per token, the wave's TM x values; the reads of batch b + 1
-// are issued before batch b is computed (two register sets).
-template <int TM, int TE, int KC>
+// are issued before batch b is computed (two register sets).  TWO: the grid
+// has at least two blocks per CU, and the chunk ring is sized so that two
+// blocks share a CU's LDS (one wave per SIMD leaves the LDS latency exposed).
+template <int TM, int TE, int KC, bool TWO>
 __global__ __launch_bounds__(256) void route_logits_kernel(const uint16_t* __restrict__ x,
                                                            const float* __restrict__ w,
                                                            const float* __restrict__ bias,
@@ -55,9 +57,10 @@ __global__ __launch_bounds__(256) void route_logits_kernel(const uint16_t* __res
   constexpr int XPL = 1024 / (KC * 2);        // token rows per 1 KiB x load
   constexpr int LPWX = (TB + 4 * XPL - 1) / (4 * XPL);  //                      x
   constexpr int CHUNK = WCH + LPWX * 4 * 1024;  // W_r rows, then the token rows
-  constexpr int NBUF = 4 * CHUNK <= 160 * 1024 ? 4 : 3;
+  constexpr int LDS_CAP = TWO ? 80 * 1024 : 160 * 1024;
+  constexpr int NBUF = 4 * CHUNK <= LDS_CAP ? 4 : 3 * CHUNK <= LDS_CAP ? 3 : 2;
   static_assert(KC % 8 == 0 && WCH % 4096 == 0 && (KC * 2) <= 1024 && 1024 % (KC * 2) == 0 &&
-                    NBUF * CHUNK <= 160 * 1024,
+                    NBUF * CHUNK <= LDS_CAP,
                 "chunk shape");
   __shared__ __align__(16) char ws[NBUF * CHUNK];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -240,14 +243,30 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   }
 }
 
+int router_cus() {
+  static int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      n = 256;
+    return n;
+  }();
+  return cus;
+}
+
 template <int TM, int TE>
 hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                       int E, float* logits, hipStream_t s) {
   // chunk rows: KC * TE a multiple of 16 (whole 4 KiB per chunk buffer)
   constexpr int KC = TE == 1 ? 128 : TE == 2 ? 64 : TE == 4 ? 32 : TE <= 8 ? 16 : 8;
-  const unsigned grid = static_cast<unsigned>(ceil_div(T, 4 * TM));
+  const int64_t grid = ceil_div(T, 4 * TM);
   prof_begin(K_ROUTE_LOGITS, s);
-  route_logits_kernel<TM, TE, KC><<<grid, 256, 0, s>>>(x, w, bias, T, d, E, logits);
+  if (grid >= 2 * static_cast<int64_t>(router_cus()))
+    route_logits_kernel<TM, TE, KC, true><<<static_cast<unsigned>(grid), 256, 0, s>>>(
+        x, w, bias, T, d, E, logits);
+  else
+    route_logits_kernel<TM, TE, KC, false><<<static_cast<unsigned>(grid), 256, 0, s>>>(
+        x, w, bias, T, d, E, logits);
   prof_end(K_ROUTE_LOGITS, s);
   return hipGetLastError();
 }
