@@ -271,18 +271,18 @@ hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int6
   return hipGetLastError();
 }
 
-// Tokens per wave: about one block per CU (T / 1024 tokens per wave,
-// rounded down to 8, 4, 2 or 1), so that every block reads W_r once for as
-// many tokens as the chip's share allows, with at most 64 accumulators per
-// lane (TM * TE <= 64).
+// Tokens per wave: about two blocks per CU (T / 2048 tokens per wave,
+// rounded down to 8, 4, 2 or 1), so that two waves share each SIMD while
+// every block still reads W_r for as many tokens as the chip's share allows,
+// with at most 64 accumulators per lane (TM * TE <= 64).
 template <int TE>
 hipError_t pick_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                        int E, float* logits, hipStream_t s) {
   if constexpr (8 * TE <= 64)
-    if (T >= 8 * 1024) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
+    if (T >= 16 * 1024) return run_logits<8, TE>(x, w, bias, T, d, E, logits, s);
   if constexpr (4 * TE <= 64)
-    if (T >= 4 * 1024) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
-  if (T >= 2 * 1024) return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
+    if (T >= 8 * 1024) return run_logits<4, TE>(x, w, bias, T, d, E, logits, s);
+  if (T >= 4 * 1024) return run_logits<2, TE>(x, w, bias, T, d, E, logits, s);
   return run_logits<1, TE>(x, w, bias, T, d, E, logits, s);
 }
 
