@@ -1,6 +1,7 @@
 // C ABI of the MoE library: argument validation (pure host code, run before
 // any HIP call), workspace queries, status strings and the optional
 // per-kernel event profiler.  Kernels live in route/permute/combine/gemm.hip.
+#include <atomic>
 #include <cstdio>
 #include <mutex>
 #include <string>
@@ -92,6 +93,18 @@ const char* const kNames[moe::K_NUM] = {
 }  // namespace
 
 namespace moe {
+int device_cus() {
+  constexpr int kMaxDev = 64;
+  static std::atomic<int> cache[kMaxDev];
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (dev >= 0 && dev < kMaxDev && (n = cache[dev].load(std::memory_order_relaxed)) > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  if (dev >= 0 && dev < kMaxDev) cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
 void prof_begin(int id, hipStream_t s) {
   Prof& p = prof();
   if (!p.on) return;

@@ -94,6 +94,10 @@ enum KernelId {
 void prof_begin(int id, hipStream_t s);
 void prof_end(int id, hipStream_t s);
 
+// Compute units of the current device (cached per device; 256 if the
+// query fails).
+int device_cus();
+
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

@@ -1150,14 +1150,7 @@ hipError_t run_gemm(const GemmArgs& a, int64_t blocks, int kid, hipStream_t s) {
 
 // Persistent grid: one workgroup per CU (a multiple of the 8 XCDs).
 int64_t pgrid() {
-  static int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      n = 256;
-    return n;
-  }();
-  const int64_t g = (cus / NXCD) * NXCD;
+  const int64_t g = (device_cus() / NXCD) * NXCD;
   return g > 0 ? g : NXCD;
 }
 

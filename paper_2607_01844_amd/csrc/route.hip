@@ -243,17 +243,6 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   }
 }
 
-int router_cus() {
-  static int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      n = 256;
-    return n;
-  }();
-  return cus;
-}
-
 template <int TM, int TE>
 hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int64_t T, int d,
                       int E, float* logits, hipStream_t s) {
@@ -261,7 +250,7 @@ hipError_t run_logits(const uint16_t* x, const float* w, const float* bias, int6
   constexpr int KC = TE == 1 ? 128 : TE == 2 ? 64 : TE == 4 ? 32 : TE <= 8 ? 16 : 8;
   const int64_t grid = ceil_div(T, 4 * TM);
   prof_begin(K_ROUTE_LOGITS, s);
-  if (grid >= 2 * static_cast<int64_t>(router_cus()))
+  if (grid >= 2 * static_cast<int64_t>(device_cus()))
     route_logits_kernel<TM, TE, KC, true><<<static_cast<unsigned>(grid), 256, 0, s>>>(
         x, w, bias, T, d, E, logits);
   else
