@@ -1,4 +1,4 @@
-"""Host checks of the build's bookkeeping (no GPU): the device-code hashes
+"""Host checks of the build step's bookkeeping (no GPU): the device-code hashes
 written beside the library, and the benchmark's use of them to decide
 whether a stored counter summary still describes the built GEMM kernel."""
 import json
