@@ -7,13 +7,18 @@ gradients) -> permutation backward.  Inputs are resident in HBM before the
 timed region starts.  A second timed loop adds the router backward (dW_r,
 dbias and the router's share of dx) to every step: "with_router_backward".
 
-Prints ONE JSON line (rank 0).  Default workload: T=4096 tokens, d=2048,
-E=64 experts, top-6, f=1408 SwiGLU (bf16, fp32 router, seed 0).  Besides the
-step it reports, each under its own key: per-kernel times and roofline
-fractions, the memory-efficient (chunked) forward, the vendor batched GEMM
-on the same six products (context), least-loaded expert parallelism on the
-skewed workload's routing, the blockwise vocabulary loss, and the CPU
-oracle's rate on a bounded sample.
+Prints ONE JSON line (rank 0).  Default workload: the long-context chunk,
+T=65536 tokens, d=4096, E=128 experts, top-8, f=1536 SwiGLU, 8 hot experts
+taking half of the assignments (bf16, fp32 router, seed 0): the largest
+configuration that fits one GPU.  `value` is T over the mean step time of the
+K timed steps; the median and minimum of the per-step times are reported
+beside it.  Besides the step it reports, each under its own key: per-kernel
+times and roofline fractions (a pass with a 512 MiB cache-flushing write
+before every step), the other workloads' steps, the memory-efficient
+(chunked) forward, the vendor batched GEMM on the same six products
+(context), least-loaded expert parallelism on the skewed workload's routing,
+the blockwise vocabulary loss, and the CPU oracle's rate on a bounded
+sample.
 """
 from __future__ import annotations
 
@@ -32,7 +37,7 @@ import torch  # noqa: E402
 import workloads as W  # noqa: E402
 
 METRIC = "MoE layer fwd+bwd tokens/s and grouped-GEMM TFLOP/s (% bf16 MFMA peak)"
-PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 4096 FLOP/clk x 2.4 GHz
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 GEMM_KERNELS = ("gemm_fwd_gate_up", "gemm_fwd_down", "gemm_dgrad_down", "gemm_dgrad_gate_up",
                 "gemm_wgrad_gate_up", "gemm_wgrad_down")
@@ -357,6 +362,17 @@ def vocab_loss(steps: int, warmup: int):
             "kernels": ks}
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, inp, budget_s: float):
     """The oracle (as is) on the first T_s tokens of the same workload."""
     import oracle
@@ -382,9 +398,103 @@ def cpu_baseline(wl, inp, budget_s: float):
         dt = run(ts)
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": round(ts / dt, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "sample_tokens": ts, "wall_s": round(dt, 2),
             "sample": f"fp32 oracle fwd+bwd (routing, permutation, expert FFN, combine, all "
-                      f"gradients) on the first {ts} of {wl.T} tokens with the full expert "
-                      f"weights; {dt:.1f} s wall"}
+                      f"gradients) on the first {ts} of {wl.T} tokens of {wl.name} with the "
+                      f"full expert weights; {dt:.1f} s wall on {threads} threads"}
+
+
+def time_steps(fn, steps: int):
+    """HIP events around each of `steps` calls on the current stream: mean
+    (first event to last), median and minimum per call, in ms."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(steps):
+        fn()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
+    return ev[0].elapsed_time(ev[steps]) / steps, float(np.median(per)), float(per.min())
+
+
+class Flush:
+    """A 512 MiB write that evicts the 256 MB Infinity Cache (and the L2s)
+    between measured steps, so that HBM-bound kernels start from HBM."""
+
+    def __init__(self):
+        self.buf = torch.empty((512 << 20) // 4, dtype=torch.float32, device="cuda")
+
+    def __call__(self):
+        self.buf.fill_(1.0)
+
+
+def warm(layer, warmup: int, with_router: bool = True):
+    """One step (with the router backward), then steps for 0.3 s so the clocks
+    leave their idle state, then the counted warmup steps.  None of this is
+    timed."""
+    layer.step()
+    if with_router:
+        layer.router_bwd()
+    torch.cuda.synchronize()
+    t_end = time.perf_counter() + 0.3
+    while time.perf_counter() < t_end:
+        layer.step()
+        torch.cuda.synchronize()
+    for _ in range(warmup):
+        layer.step()
+    torch.cuda.synchronize()
+
+
+def profile_pass(layer, steps: int, flush):
+    """Per-kernel times from the library's event profiler over `steps` steps
+    (router backward included), the caches flushed before every step."""
+    m = layer.moe
+    m.profile_reset()
+    for _ in range(steps):
+        flush()
+        m.profile_enable(True)
+        layer.step()
+        layer.router_bwd()
+        m.profile_enable(False)
+    torch.cuda.synchronize()
+    prof = m.profile_query()
+    m.profile_reset()
+    return prof
+
+
+def layer_stats(layer):
+    off = layer.pm["expert_offsets"].cpu().numpy()
+    dst = layer.pm["dst"].cpu().numpy()
+    return int(off[-1]), np.diff(off), int((dst >= 0).any(1).sum())
+
+
+def other_config(name: str, steps: int, warmup: int, flush):
+    """Step time, GEMM rate and roofline of one more workload (each its own
+    inputs and buffers, freed afterwards)."""
+    wl = W.WORKLOADS[name]
+    inp = W.make_inputs(wl, seed=0, device="cuda")
+    layer = Layer(wl, inp)
+    warm(layer, warmup)
+    mean, med, mn = time_steps(layer.step, steps)
+    mean_rb, _, _ = time_steps(lambda: (layer.step(), layer.router_bwd()), steps)
+    M, cnt, T_touched = layer_stats(layer)
+    prof = profile_pass(layer, steps, flush)
+    kernels, flops, _ = kernel_table(wl, M, T_touched, prof, steps)
+    gemm_ms = sum(prof[n][0] for n in GEMM_KERNELS if n in prof) / steps
+    gemm_tf = 18.0 * M * wl.d * wl.f / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else None
+    out = {"config": {**wl.describe(), "M": M, "load": W.load_stats(cnt)},
+           "ms_per_step": round(mean, 4), "median_ms": round(med, 4), "min_ms": round(mn, 4),
+           "tokens_per_s": round(wl.T / (mean * 1e-3), 1),
+           "with_router_backward_ms": round(mean_rb, 4),
+           "grouped_gemm_tflops": None if gemm_tf is None else round(gemm_tf, 1),
+           "grouped_gemm_frac_bf16_peak": None if gemm_tf is None
+           else round(gemm_tf / PEAK_BF16_TFLOPS, 4),
+           "kernels": {k: v for k, v in kernels.items()
+                       if "frac_bf16_peak" in v or "frac_hbm_peak" in v}}
+    del layer, inp
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -392,7 +502,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="mid", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--workload", default="long", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--others", default="mid,large_skew,ep_share,tiny",
+                    help="comma-separated workloads also measured (under 'configs'); '' = none")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--no-kernel-timing", action="store_true")
@@ -401,6 +513,8 @@ def main():
                     help="skip the least-loaded expert-parallelism leg")
     ap.add_argument("--no-vendor", action="store_true",
                     help="skip the vendor batched-GEMM context measurement")
+    ap.add_argument("--no-chunked", action="store_true",
+                    help="skip the memory-efficient forward leg")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
@@ -415,62 +529,25 @@ def main():
     log(f"[bench] workload {wl.describe()}")
     inp = W.make_inputs(wl, seed=0, device="cuda")
     layer = Layer(wl, inp)
-    # the router backward's first call creates the device's rocBLAS handle
-    # (a few hundred ms of host work, once per process); the GPU idles
-    # meanwhile, so steps run for a fixed 0.3 s before the counted warmup to
-    # bring its clocks back up.  None of this is timed.
-    layer.step()
-    layer.router_bwd()
-    torch.cuda.synchronize()
-    t_end = time.perf_counter() + 0.3
-    while time.perf_counter() < t_end:
-        layer.step()
-        torch.cuda.synchronize()
-    for _ in range(args.warmup):
-        layer.step()
-    torch.cuda.synchronize()
+    flush = Flush()
+    warm(layer, args.warmup)
     log("[bench] warmup done")
 
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # the timed region: K steps bracketed by synchronisations
     torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        layer.step()
-    stop.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
+    ms, med, mn = time_steps(layer.step, args.steps)
     tok_s = wl.T / (ms * 1e-3)
-    log(f"[bench] {ms:.3f} ms/step, {tok_s:.0f} tokens/s")
+    log(f"[bench] {ms:.3f} ms/step (median {med:.3f}, min {mn:.3f}), {tok_s:.0f} tokens/s")
 
     # the same step followed by the router backward (whole-layer dx, dW_r)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        layer.step()
-        layer.router_bwd()
-    stop.record()
-    torch.cuda.synchronize()
-    ms_rb = start.elapsed_time(stop) / args.steps
+    ms_rb, med_rb, mn_rb = time_steps(lambda: (layer.step(), layer.router_bwd()), args.steps)
     log(f"[bench] with router backward {ms_rb:.3f} ms/step")
 
-    off = layer.pm["expert_offsets"].cpu().numpy()
-    M = int(off[-1])
-    cnt = np.diff(off)
-    dst = layer.pm["dst"].cpu().numpy()
-    T_touched = int((dst >= 0).any(1).sum())
+    M, cnt, T_touched = layer_stats(layer)
 
     kernels, gemm_tflops, roof = {}, None, None
     if not args.no_kernel_timing:
-        m = layer.moe
-        m.profile_reset()
-        m.profile_enable(True)
-        for _ in range(args.steps):
-            layer.step()
-            layer.router_bwd()
-        torch.cuda.synchronize()
-        m.profile_enable(False)
-        prof = m.profile_query()
-        m.profile_reset()
+        prof = profile_pass(layer, args.steps, flush)
         kernels, flops, _ = kernel_table(wl, M, T_touched, prof, args.steps)
         gemm_ms = sum(prof[n][0] for n in GEMM_KERNELS if n in prof) / args.steps
         gemm_tflops = 18.0 * M * wl.d * wl.f / (gemm_ms * 1e-3) / 1e12
@@ -478,7 +555,8 @@ def main():
         avg_s = prof[dom][0] / prof[dom][1] * 1e-3
         ach = flops[dom] / avg_s / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1),
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                 "traffic": stored_traffic(wl.name, dom), "traffic_unit": "bytes per launch",
                 "avg_us": round(avg_s * 1e6, 2),
                 "work_per_launch": f"{flops[dom]:.4g} FLOP"}
@@ -492,16 +570,25 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    memfwd = chunked_forward(layer, args.steps)
-    log(f"[bench] memory-efficient forward: {memfwd}")
+    memfwd = None
+    if not args.no_chunked:
+        memfwd = chunked_forward(layer, args.steps)
+        log(f"[bench] memory-efficient forward: {memfwd}")
 
+    del layer
+    torch.cuda.empty_cache()
     vendor = None
     if not args.no_vendor:
         vendor = vendor_batched(wl, args.steps)
         log(f"[bench] vendor batched GEMM (uniform rows, context): {vendor['all_six']}")
+        torch.cuda.empty_cache()
 
-    del layer
-    torch.cuda.empty_cache()
+    configs = {}
+    for name in [n for n in args.others.split(",") if n and n != wl.name]:
+        configs[name] = other_config(name, args.steps, args.warmup, flush)
+        log(f"[bench] {name}: {configs[name]['ms_per_step']} ms/step, "
+            f"GEMMs {configs[name]['grouped_gemm_tflops']} TFLOP/s")
+
     llep = None
     if not args.no_llep:
         llep = llep_leg(args.steps)
@@ -522,6 +609,7 @@ def main():
     out = {
         "metric": METRIC, "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "median_ms_per_step": round(med, 4), "min_ms_per_step": round(mn, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; random-init weights)",
         "config": {**wl.describe(), "M": M, "tokens_with_local_slot": T_touched,
@@ -529,15 +617,17 @@ def main():
         "grouped_gemm_tflops": None if gemm_tflops is None else round(gemm_tflops, 1),
         "grouped_gemm_frac_bf16_peak": None if gemm_tflops is None
         else round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
-        "with_router_backward": {"ms_per_step": round(ms_rb, 4),
+        "with_router_backward": {"ms_per_step": round(ms_rb, 4), "median_ms": round(med_rb, 4),
+                                 "min_ms": round(mn_rb, 4),
                                  "value": round(wl.T / (ms_rb * 1e-3), 1), "unit": "tokens/s"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "configs": configs,
         "memory_efficient_forward": memfwd,
         "llep": llep,
         "vocab_loss": voc,
         "vendor_batched_gemm_context": vendor,
-        "roofline": roof,
-        "cpu_baseline": cpu,
-        "kernels": kernels,
         "device": torch.cuda.get_device_name(0),
     }
     print(json.dumps(out), flush=True)

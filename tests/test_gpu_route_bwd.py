@@ -186,3 +186,47 @@ def test_route_bwd_full_size(name):
     errs["dx_sampled"] = P.assert_close("dx (sampled tokens)", P.f64(dx[torch.as_tensor(
         tt, device="cuda")]), ref_dx)
     _say(f"[route_bwd] {name} ok {errs}")
+
+
+CHAIN = [
+    # name, workload, router bias (None = no bias)
+    ("chain_small", W.Workload("chain_small", T=300, d=136, E=12, k=3, f=72), 0.1),
+    ("chain_renorm", W.Workload("chain_renorm", T=256, d=64, E=8, k=2, f=48, renorm=1), None),
+    # T*d*E = 2^28: the router backward takes its matrix-core path
+    ("chain_mfma", W.Workload("chain_mfma", T=2048, d=1024, E=128, k=6, f=64), 0.1),
+]
+
+
+@pytest.mark.parametrize("case", CHAIN, ids=[c[0] for c in CHAIN])
+def test_route_bwd_oracle_chain(case):
+    """Closed loop: the reference comes from the oracle alone, started from
+    the original inputs (its forward's logits, routing, gates, gate
+    gradients and expert-path dx, then its fp64 router backward on those);
+    the HIP side runs the whole layer and moe_route_bwd on its own
+    intermediates.  The whole layer's dx and dW_r, dbias are compared at the
+    layer-wide 1e-2 (the HIP gate gradients carry the bf16 rounding of
+    y_perm)."""
+    from tests.test_gpu_parity import make, run_layer
+    name, wl, bias_std = case
+    _say(f"[route_bwd] {name} {wl.describe()}")
+    bias = None
+    if bias_std is not None:
+        bias = (bias_std * np.random.default_rng(3).standard_normal(wl.E)).astype(np.float32)
+    inp = make(wl, bias=bias)
+    gpu = run_layer(inp, wl)
+    x, w, b = inp["x"], inp["w_router"], inp.get("router_bias")
+    lg, idx, gate = _route(x, w, b, wl.k, wl.renorm)
+    dw, db, dx, _ = _run_bwd(x, w, lg, idx, gate, gpu["dgate"], wl.renorm, gpu["dx"], True, True,
+                             False)
+    h = P.host_inputs(inp)
+    o = oracle.layer(h["x"], h["w_r"], h["bias"], h["wg"], h["wu"], h["wd"], h["dy"], wl.k,
+                     renorm=wl.renorm, prec="f32")
+    assert np.array_equal(idx.cpu().numpy(), o["topk_idx"]), "topk_idx differs"
+    ref_dw, ref_dxr, ref_db = oracle.router_bwd_f64(
+        P.f64(x), P.f64(w), o["logits"].astype(np.float64), o["topk_idx"],
+        o["topk_gate"].astype(np.float64), o["dgate"].astype(np.float64), wl.renorm)
+    errs = {"dw_router": P.assert_close("dw_router", P.f64(dw), ref_dw),
+            "dbias": P.assert_close("dbias", P.f64(db), ref_db),
+            "dx": P.assert_close("dx (whole layer)", P.f64(dx),
+                                 o["dx"].astype(np.float64) + ref_dxr)}
+    _say(f"[route_bwd] {name} ok {errs}")
