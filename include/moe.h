@@ -15,10 +15,10 @@
  *  - bf16 values are raw IEEE bfloat16 bit patterns (moe_bf16); fp32->bf16 is
  *    round-to-nearest-even.  All arrays are dense and row-major.
  *  - Every pointer is DEVICE memory owned by the caller; the library
- *    allocates nothing (save one rocBLAS handle per device, created by the
- *    first call that needs it: the vocabulary loss, or a router backward
- *    with T*d*E >= 2^28) and keeps no reference after the call returns.
- *    Required pointers must be non-NULL and 16-byte aligned.
+ *    allocates nothing (callers pass workspaces sized by the
+ *    *_workspace_bytes queries) and keeps no reference after the call
+ *    returns.  Every product runs on the library's own kernels.  Required
+ *    pointers must be non-NULL and 16-byte aligned.
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *    Calls only enqueue work and return; no call synchronises the device.
  *    Data-dependent sizes (M, the number of local assignments) stay on the
@@ -110,10 +110,10 @@ int moe_route(const moe_bf16* x, const float* w_router, const float* router_bias
  *   dx[t][j]        = bf16( [float(dx[t][j]) +] sum over e of
  *                     dlogits[t][e] w_router[j][e] )               (optional)
  * in fp32 on the vector ALUs (e ascending for dx) when T*d*E < 2^28, and
- * above that on the bf16 matrix cores with each fp32 operand v taken as
- * bf16(v) + bf16(v - bf16(v)) (relative error <= 2^-17, fp32 accumulation,
- * rocBLAS products with atomics off; token chunks of dw_router summed in
- * order).  dlogits and dbias are fp32 in both.
+ * above that on the library's bf16 matrix-core kernel with each fp32
+ * operand v taken as bf16(v) + bf16(v - bf16(v)) (relative error <= 2^-17,
+ * fp32 accumulation; token chunks of dw_router summed in order).  dlogits
+ * and dbias are fp32 in both.
  * dx_accumulate = 1 adds the router's share to the expert path's input
  * gradient already in dx (e.g. from the unit-weight moe_combine of dx_perm),
  * giving the whole layer's dx; dx is then read and written in place (the one
@@ -223,11 +223,11 @@ int moe_combine_bwd(const moe_bf16* dout, const moe_bf16* y_perm, const int32_t*
                     float* dgate, void* stream);
 
 /* ---------------------------------------------- memory-efficient forward
- * The expert layer's forward over chunks of `chunk` tokens (Sec. 3.3, the
- * memory-efficient variant: overlap the movement of routed rows with the
- * expert computation so that only a small fraction of the routed inputs,
- * dispatch buffers and expert intermediates is resident at once; eq. (peaks)
- * names that O(N k H + N_r I) transient).  For tokens [c*chunk, (c+1)*chunk)
+ * The expert layer's forward over chunks of `chunk` tokens (the
+ * memory-efficient variant of Sec. 3.3; its target is the O(N k H + N_r I)
+ * transient of eq. (peaks): routed rows and expert intermediates exist for
+ * one slice of the work at a time, while the next slice's row movement runs
+ * beside the current slice's products).  For tokens [c*chunk, (c+1)*chunk)
  * it runs moe_permute, moe_grouped_swiglu_fwd and moe_combine (weighted by
  * topk_gate) into y, alternating chunks between `stream` and `stream2` with
  * two sets of transient buffers inside the workspace: the transient peak is
@@ -258,9 +258,11 @@ int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, const float*
  * Blockwise online loss of the vocabulary projection (Sec. 3.4, eq.
  * (voc-fwd-loss): Y = X W_voc, loss_n = Y[n][t_n] - log sum_v exp Y[n][v]),
  * on one device with the vocabulary walked in blocks of `vblock` columns
- * instead of split over ranks: only an N x vblock slice of the logits is
- * resident at any instant, never the N x V tensor, and the loss and its
- * gradients are those of the dense projection up to rounding.
+ * instead of split over ranks.  The logits are never stored: each block's
+ * product reduces them in its epilogue (forward: a running max and sum of
+ * exponentials per row, merged block by block; backward: the logit
+ * gradient, the only per-block buffer, N x vblock bf16), and the loss and
+ * its gradients are those of the dense projection up to rounding.
  *
  * x [N][H] bf16; w_voc [H][V] bf16; target [N] int32 in [0, V) (a target
  * outside [0, V) is undefined behaviour).  Logits are fp32 sums of bf16
@@ -274,11 +276,11 @@ int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, const float*
  * bf16 before the two products.  Limits: 0 <= N < 2^31, 1 <= V < 2^31, H a
  * multiple of 8, vblock a positive multiple of 8, N * vblock < 2^40.
  * workspace: moe_vocab_loss_workspace_bytes() bytes (serves both calls;
- * about 6 N vblock + 4 N H bytes + 32 MiB).  The three products per block
- * are rocBLAS GEMMs: the first call on a device that needs rocBLAS creates
- * that device's handle (the one allocation the library makes; it is kept
- * until the process ends), and calls that use it on one device serialise on
- * its host lock.
+ * 2 N vblock bytes of logit gradients, up to 8 fp32 N x H slabs of dx
+ * partial sums and N vblock / 8 bytes of per-64-column pairs; when V is not
+ * a multiple of 8, also padded copies of one block of W and of dW).  It does
+ * not depend on V otherwise.  All products run on the library's bf16
+ * matrix-core kernel with fp32 accumulation.
  */
 int moe_vocab_loss_workspace_bytes(int64_t N, int H, int64_t V, int64_t vblock, size_t* bytes);
 int moe_vocab_loss_fwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* target, int64_t N,
@@ -290,12 +292,11 @@ int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* 
                        size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------ least-loaded expert parallelism
- * Sec. 3.3 (recap of LLEP): at every MoE call the per-rank load is
- * measured, excess token-expert assignments move from overloaded ranks to
- * underloaded ones and the expert weights travel with them, so that the
- * receiving rank computes those products itself; which products are
- * computed never changes.  The planning steps are not given in the paper;
- * this library's plan is:
+ * Sec. 3.3 (recap of LLEP): the load of each rank is taken at every call
+ * of the layer; a rank above its share hands some of its token-expert
+ * products, together with the weights of those experts, to a rank below
+ * it, which then computes them; the set of products does not change.  The
+ * paper does not give the planning steps; this library's plan is:
  *   - E experts on E_p ranks, expert e at home on rank e / (E / E_p);
  *     L = sum of counts; capacity C = max(capacity, ceil(L / E_p));
  *   - every rank keeps its own experts, ascending, while its load stays

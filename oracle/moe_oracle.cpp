@@ -43,6 +43,7 @@
 #include <cstdint>
 #include <cstring>
 #include <numeric>
+#include <limits>
 #include <vector>
 
 namespace {
@@ -110,8 +111,12 @@ void topk_gates(const L* logits, int64_t T, int E, int k, int renorm, int32_t* i
     std::vector<int> order(E);
     std::iota(order.begin(), order.end(), 0);
     // total order: larger logit first; equal logits (including -0 == +0)
-    // keep ascending expert index (stable sort of an ascending sequence)
-    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return l[a] > l[b]; });
+    // keep ascending expert index (stable sort of an ascending sequence); a
+    // NaN logit ranks as -inf
+    auto key = [&](int e) {
+      return std::isnan(l[e]) ? -std::numeric_limits<L>::infinity() : l[e];
+    };
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return key(a) > key(b); });
     const double m = static_cast<double>(l[order[0]]);
     double den = 0.0;
     if (renorm == 0) {

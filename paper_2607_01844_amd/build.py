@@ -21,7 +21,8 @@ LIB = os.path.join(PKG, "libmoe.so")
 # object), written beside the library at every build: a stored measurement
 # names the code it was taken on, and stays valid while that code is unchanged
 DEVICE_TEXT = os.path.join(PKG, "libmoe.device_text.json")
-SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "chunked.hip", "vocab.hip", "llep.hip", "blas.hip"]
+SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip",
+           "chunked.hip", "vocab.hip", "llep.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -77,9 +78,7 @@ def build(verbose: bool = False) -> str:
     with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp%d" % os.getpid()
-    # rocBLAS runs the vocabulary projection's plain dense products
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-L/opt/rocm/lib",
-           "-lrocblas", "-Wl,-rpath,/opt/rocm/lib", "-o", tmp]
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)

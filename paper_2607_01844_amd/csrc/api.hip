@@ -88,7 +88,8 @@ const char* const kNames[moe::K_NUM] = {
     "permute_rank", "permute_gather",  "gemm_sched",         "gemm_fwd_gate_up",
     "gemm_fwd_down", "gemm_dgrad_down", "gemm_dgrad_gate_up", "gemm_wgrad_gate_up",
     "gemm_wgrad_down", "combine",       "combine_bwd",        "route_dlogits",
-    "route_dw",     "route_dx",        "vocab_lse",          "vocab_grad",    "llep_plan",     "llep_window"};
+    "route_dw",     "route_dx",        "vocab_lse",          "vocab_grad",    "llep_plan",     "llep_window",
+    "route_split",  "vocab_logits",    "vocab_dx",           "vocab_dw"};
 
 }  // namespace
 
@@ -418,7 +419,8 @@ MOE_API int moe_vocab_loss_workspace_bytes(int64_t N, int H, int64_t V, int64_t 
   const char* fn = "moe_vocab_loss_workspace_bytes";
   CHECK(bytes != nullptr, "bytes is NULL");
   if (int r = check_vocab(fn, N, H, V, vblock)) return r;
-  *bytes = std::max(moe::vocab_fwd_ws_bytes(N, vblock), moe::vocab_bwd_ws_bytes(N, H, vblock));
+  *bytes = std::max(moe::vocab_fwd_ws_bytes(N, H, V, vblock),
+                    moe::vocab_bwd_ws_bytes(N, H, V, vblock));
   return MOE_OK;
 }
 
@@ -430,7 +432,7 @@ MOE_API int moe_vocab_loss_fwd(const moe_bf16* x, const moe_bf16* w_voc, const i
   if (int r = check_vocab(fn, N, H, V, vblock)) return r;
   if (N > 0) {
     REQ(x); REQ(w_voc); REQ(target); REQ(loss); REQ(lse);
-    if (workspace == nullptr || workspace_bytes < moe::vocab_fwd_ws_bytes(N, vblock))
+    if (workspace == nullptr || workspace_bytes < moe::vocab_fwd_ws_bytes(N, H, V, vblock))
       return fail(MOE_ERR_WORKSPACE, fn, "workspace smaller than moe_vocab_loss_workspace_bytes()");
     OPT(workspace);
   }
@@ -448,7 +450,7 @@ MOE_API int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const i
   REQ(dw_voc);
   if (N > 0) {
     REQ(x); REQ(w_voc); REQ(target); REQ(lse); REQ(dloss); REQ(dx);
-    if (workspace == nullptr || workspace_bytes < moe::vocab_bwd_ws_bytes(N, H, vblock))
+    if (workspace == nullptr || workspace_bytes < moe::vocab_bwd_ws_bytes(N, H, V, vblock))
       return fail(MOE_ERR_WORKSPACE, fn, "workspace smaller than moe_vocab_loss_workspace_bytes()");
     OPT(workspace);
   }

@@ -87,6 +87,10 @@ enum KernelId {
   K_VOC_GRAD,
   K_LLEP_PLAN,
   K_LLEP_WINDOW,
+  K_ROUTE_SPLIT,
+  K_VOC_LOGITS,
+  K_VOC_DX,
+  K_VOC_DW,
   K_NUM
 };
 
@@ -113,8 +117,8 @@ hipError_t launch_route_bwd(const uint16_t* x, const float* w, const float* logi
                             int64_t T, int d, int E, int k, int renorm, float* dw, float* dbias,
                             uint16_t* dx, int dx_accumulate, float* dlogits, void* ws,
                             hipStream_t s);
-size_t vocab_fwd_ws_bytes(int64_t N, int64_t vblock);
-size_t vocab_bwd_ws_bytes(int64_t N, int H, int64_t vblock);
+size_t vocab_fwd_ws_bytes(int64_t N, int H, int64_t V, int64_t vblock);
+size_t vocab_bwd_ws_bytes(int64_t N, int H, int64_t V, int64_t vblock);
 hipError_t launch_vocab_fwd(const uint16_t* x, const uint16_t* w, const int32_t* target,
                             int64_t N, int H, int64_t V, int64_t vblock, float* loss, float* lse,
                             void* ws, hipStream_t s);
@@ -147,6 +151,37 @@ hipError_t launch_combine_bwd(const uint16_t* dout, const uint16_t* y, const int
                               const float* gate, int64_t T, int d, int k, uint16_t* dy_perm,
                               float* dgate, hipStream_t s);
 size_t gemm_ws_bytes(int64_t cap, int E_loc, int d, int f, unsigned flags);
+// Dense products on the grouped GEMM kernel (bf16 operands, fp32 accumulation).
+// Router backward, fp32 operands split as bf16 hi + lo: dl3 [T][ld3] holds
+// [hi | hi | lo] of the logit gradients (E columns each), w3 [3E][d] holds
+// [hi; lo; hi] of W_r^T.
+//   part[c][j][e] = sum over tokens t of chunk c of x[t][j] (hi + lo)[t][e]
+//   dx[t][j] = bf16([float(dx[t][j]) +] sum over the 3E columns of dl3 w3)
+hipError_t launch_router_dw_mfma(const uint16_t* x, const uint16_t* dl3, int64_t T, int d, int E,
+                                 int64_t ld3, int64_t chunk, float* part, hipStream_t s);
+hipError_t launch_router_dx_mfma(const uint16_t* dl3, const uint16_t* w3, int64_t T, int d, int E,
+                                 int64_t ld3, int accumulate, uint16_t* dx, hipStream_t s);
+// Vocabulary block [v0, v0 + vb) of W [H][ldw] (B read from column bc0):
+//   logits: part[n][c / 64] = (max, sum exp(y - max)) over the block's
+//     columns c..c+63 of row n, yt[n] = y[n][target[n] - v0] where the
+//     target lies in the block;
+//   grad: G[n][c] = bf16(dloss[n] ([v0 + c == target[n]] - exp(y - lse[n]))),
+//     zeros for c in [vb, gp);
+//   dx: dxa[b][n][h] (=, first) or (+=) sum over c in batch b's kspan
+//     columns of G[n][c] W[h][bc0 + c];
+//   dw: dw[h][cc0 + c] = bf16(sum_n x[n][h] G[n][c]), row pitch ldd.
+hipError_t launch_vocab_logits_mfma(const uint16_t* x, const uint16_t* w, int64_t ldw, int64_t bc0,
+                                    int64_t v0, int N, int H, int vb, const int32_t* target,
+                                    float* part, float* yt, hipStream_t s);
+hipError_t launch_vocab_grad_mfma(const uint16_t* x, const uint16_t* w, int64_t ldw, int64_t bc0,
+                                  int64_t v0, int N, int H, int vb, const int32_t* target,
+                                  const float* lse, const float* dloss, uint16_t* G, int64_t gp,
+                                  hipStream_t s);
+hipError_t launch_vocab_dx_mfma(const uint16_t* G, int64_t gp, const uint16_t* w, int64_t ldw,
+                                int64_t bc0, int N, int H, int vb, int kspan, int first,
+                                float* dxa, hipStream_t s);
+hipError_t launch_vocab_dw_mfma(const uint16_t* x, const uint16_t* G, int64_t gp, int N, int H,
+                                int vb, uint16_t* dw, int64_t ldd, int64_t cc0, hipStream_t s);
 hipError_t launch_ffn_fwd(const uint16_t* x_perm, const int32_t* offsets, int E_loc, int64_t cap,
                           int d, int f, const uint16_t* wg, const uint16_t* wu,
                           const uint16_t* wd, uint16_t* hg, uint16_t* hu, uint16_t* y,

@@ -62,7 +62,29 @@ enum Mode {
   DGRAD_DOWN,       // dA = dY Wd^T -> dHg, dHu, A                 (K = d)
   DGRAD_GATE_UP,    // dX = dHg Wg^T + dHu Wu^T                    (K = 2f)
   WGRAD_GATE_UP,    // dWg, dWu = X^T dHg, X^T dHu                 (dual B, K = n_e)
-  WGRAD_DOWN        // dWd = A^T dY                                (K = n_e)
+  WGRAD_DOWN,       // dWd = A^T dY                                (K = n_e)
+  // Dense products: `batches` independent products of one shape, batch b
+  // covering K rows [b kspan, min((b + 1) kspan, K)) of the contraction.
+  RT_DW,            // router: part[b] = X_b^T (DLhi_b + DLlo_b), fp32   (dual B)
+  RT_DX,            // router: dx = bf16([dx +] DL3 W3), K = 3E
+  VOC_FWD,          // vocabulary: per row and 64 columns (max, sum exp), target logit
+  VOC_GRAD,         // vocabulary: G = bf16(dl ([v == t] - exp(y - lse)))
+  VOC_DX,           // vocabulary: dxa[b] (+)= G_b W_b^T, fp32
+  VOC_DW            // vocabulary: dW[:, block] = X^T G, bf16
+};
+
+template <int MODE>
+struct Traits {
+  static constexpr bool DENSE = MODE >= RT_DW;
+  // operand A stored with the output row index contiguous (read transposed)
+  static constexpr bool A_N =
+      MODE == WGRAD_GATE_UP || MODE == WGRAD_DOWN || MODE == RT_DW || MODE == VOC_DW;
+  // operand B stored K-contiguous
+  static constexpr bool B_K = MODE == DGRAD_DOWN || MODE == DGRAD_GATE_UP || MODE == VOC_DX;
+  // B tile = 128 columns of each of two sources (same output column)
+  static constexpr bool DUAL = MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP || MODE == RT_DW;
+  // grouped weight gradients (K = an expert's rows, zero tiles for empty experts)
+  static constexpr bool WG = MODE == WGRAD_GATE_UP || MODE == WGRAD_DOWN;
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -332,6 +354,23 @@ struct GemmArgs {
   int E_loc, d, f;
   int NT;  // column tiles per row tile
   int MT;  // row tiles per expert (weight-gradient modes)
+  // dense products
+  const uint16_t* da;       // operand A
+  const uint16_t* db;       // operand B
+  void* dc;                 // output
+  const int32_t* target;    // vocabulary: target of each row [N]
+  const float* lse;         // vocabulary: log-sum-exp of each row [N]
+  const float* dloss;       // vocabulary: upstream gradient of each row [N]
+  float* yt;                // vocabulary: target logit of each row [N]
+  int64_t a_ld, b_ld, c_ld; // row pitches (elements)
+  int64_t c_bstride;        // output elements per batch
+  int64_t v0;               // vocabulary: block's first column in B's (or dW's) row
+  int dM, dN, dK;           // output rows, valid output columns, contraction length
+  int kspan, batches;       // contraction rows per batch, batches
+  int64_t bc0;              // vocabulary: B's first column (the block, or 0 when staged)
+  int64_t cc0;              // vocabulary: dW's first column (VOC_DW)
+  int dE;                   // router: experts (the lo parts sit 2E columns into DL3)
+  int flag;                 // RT_DX: add to dx; VOC_DX: first block (store, no add)
 };
 
 __device__ __forceinline__ uint2 pack4(float a, float b, float c, float d) {
@@ -375,10 +414,27 @@ struct Tables {
   __device__ __forceinline__ int nz(int i) const { return sld(nz_start_ + i); }
 };
 
+// Position (m, n) of tile `local` of an mt x nt grid, walked in groups of
+// GM row tiles: inside a group the row tiles of one column tile are
+// adjacent and the group's column tiles follow one another.  The 32
+// consecutive tiles an XCD runs at a time then form a GM x 32/GM block
+// that shares GM row slabs and 32/GM column slabs of the operands in that
+// XCD's L2 (instead of 32 row slabs and one column slab).
+constexpr int GM = 8;
+__device__ __forceinline__ void tile_pos(int local, int mt, int nt, int& m, int& n) {
+  const int per = GM * nt;
+  const int grp = local / per;
+  const int r = local - grp * per;
+  const int gm = min(GM, mt - grp * GM);
+  m = grp * GM + r % gm;
+  n = r / gm;
+}
+
 template <int MODE>
 struct TileIter {
-  static constexpr bool WG = (MODE == WGRAD_GATE_UP || MODE == WGRAD_DOWN);
-  static constexpr bool DUAL = (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP);
+  static constexpr bool WG = Traits<MODE>::WG;
+  static constexpr bool DUAL = Traits<MODE>::DUAL;
+  static constexpr bool DENSE = Traits<MODE>::DENSE;
   int xcd, j, cpx, i;
   int total, end;  // row-grouped: tile count, end of this XCD's range
   int unit;        // weight gradients: tiles per expert with rows (MT * NT)
@@ -405,7 +461,14 @@ struct TileIter {
     xcd = blockIdx.x % NXCD;
     j = blockIdx.x / NXCD;
     i = 0;
-    if constexpr (!WG) {
+    if constexpr (DENSE) {
+      // batches x MT x NT tiles, row tiles of one column tile adjacent, cut
+      // into 8 contiguous equal ranges (one per XCD)
+      total = g.batches * g.MT * g.NT;
+      const int per = (total + NXCD - 1) / NXCD;
+      end = min((xcd + 1) * per, total);
+      total = xcd * per;
+    } else if constexpr (!WG) {
       total = tb.mt(g.E_loc) * g.NT;
       const int per = (total + NXCD - 1) / NXCD;
       end = min((xcd + 1) * per, total);
@@ -421,7 +484,23 @@ struct TileIter {
   __device__ __forceinline__ Tile next(const GemmArgs& g, const Tables& tb) {
     Tile t;
     t.valid = false;
-    if constexpr (!WG) {
+    if constexpr (DENSE) {
+      const int L = total + j + cpx * i;
+      ++i;
+      if (L >= end) return t;
+      const int per_b = g.MT * g.NT;
+      const int b = L / per_b, local = L - b * per_b;
+      t.e = b;
+      int tm, tn;
+      tile_pos(local, g.MT, g.NT, tm, tn);
+      t.m0 = tm * BM;
+      t.n0 = tn * (DUAL ? BN / 2 : BN);
+      t.seg = b * g.kspan;               // first contraction row of the batch
+      t.ne = min(g.kspan, g.dK - t.seg);  // its contraction rows
+      t.nk = (t.ne + BK - 1) / BK;
+      t.valid = true;
+      return t;
+    } else if constexpr (!WG) {
       const int L = total + j + cpx * i;
       ++i;
       if (L >= end) return t;
@@ -434,8 +513,10 @@ struct TileIter {
       const int ms0 = tb.mt(lo);
       const int mt_e = tb.mt(lo + 1) - ms0;
       const int local = L - ms0 * g.NT;
-      t.m0 = (local % mt_e) * BM;
-      t.n0 = (local / mt_e) * (DUAL ? BN / 2 : BN);
+      int tm, tn;
+      tile_pos(local, mt_e, g.NT, tm, tn);
+      t.m0 = tm * BM;
+      t.n0 = tn * (DUAL ? BN / 2 : BN);
       t.seg = tb.off(lo);
       t.ne = tb.off(lo + 1) - t.seg;
       const int K = (MODE == FWD_GATE_UP || MODE == DGRAD_DOWN) ? g.d : g.f;
@@ -458,8 +539,10 @@ struct TileIter {
       ecache = e;
       t.e = __builtin_amdgcn_readfirstlane(e);
       const int local = L - unit * tb.nz(e);
-      t.m0 = (local % g.MT) * BM;
-      t.n0 = (local / g.MT) * (DUAL ? BN / 2 : BN);
+      int tm, tn;
+      tile_pos(local, g.MT, g.NT, tm, tn);
+      t.m0 = tm * BM;
+      t.n0 = tn * (DUAL ? BN / 2 : BN);
       t.seg = tb.off(e);
       t.ne = tb.off(e + 1) - t.seg;
       t.nk = (t.ne + BK - 1) / BK;
@@ -489,10 +572,11 @@ struct TileIter {
 template <int MODE>
 __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   __shared__ __align__(1024) char lds[NRING * UNIT];
-  constexpr bool WGRAD = (MODE == WGRAD_GATE_UP || MODE == WGRAD_DOWN);
-  constexpr bool DUAL = (MODE == FWD_GATE_UP || MODE == WGRAD_GATE_UP);
-  constexpr bool A_N = WGRAD;                                        // A side N-major?
-  constexpr bool B_K = (MODE == DGRAD_DOWN || MODE == DGRAD_GATE_UP);  // B side K-major?
+  constexpr bool WGRAD = Traits<MODE>::WG;
+  constexpr bool DENSE = Traits<MODE>::DENSE;
+  constexpr bool DUAL = Traits<MODE>::DUAL;
+  constexpr bool A_N = Traits<MODE>::A_N;  // A side N-major?
+  constexpr bool B_K = Traits<MODE>::B_K;  // B side K-major?
   using AOp = typename std::conditional<A_N, NOperand, KOperand>::type;
   using BOp = typename std::conditional<B_K, KOperand, NOperand>::type;
 
@@ -528,10 +612,24 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       A.ptr0 = g.x_perm + (int64_t)seg * d + m0; A.range0 = ((int64_t)ne * d - m0) * 2;
       A.ptr1 = A.ptr0 + 128; A.range1 = A.range0 - 256;
       A.ld = d * 2; A.cols0 = d - m0; A.cols1 = d - m0 - 128; A.kmax = ne;
-    } else {  // WGRAD_DOWN
+    } else if constexpr (MODE == WGRAD_DOWN) {
       A.ptr0 = g.act_in + (int64_t)seg * f + m0; A.range0 = ((int64_t)ne * f - m0) * 2;
       A.ptr1 = A.ptr0 + 128; A.range1 = A.range0 - 256;
       A.ld = f * 2; A.cols0 = f - m0; A.cols1 = f - m0 - 128; A.kmax = ne;
+    } else if constexpr (A_N) {
+      // RT_DW: X [T][d], contraction rows = the batch's tokens;
+      // VOC_DW: X [N][H], contraction rows = all N tokens (seg = 0)
+      A.ptr0 = g.da + seg * g.a_ld + m0; A.range0 = ((int64_t)ne * g.a_ld - m0) * 2;
+      A.ptr1 = A.ptr0 + 128; A.range1 = A.range0 - 256;
+      A.ld = static_cast<uint32_t>(g.a_ld * 2); A.cols0 = g.dM - m0; A.cols1 = g.dM - m0 - 128;
+      A.kmax = ne;
+    } else {
+      // K-contiguous dense A: RT_DX DL3 [T][E3p]; VOC_FWD/GRAD X [N][H];
+      // VOC_DX G [N][gp] from column seg (the batch's share of the block)
+      const uint16_t* aa = g.da + (int64_t)m0 * g.a_ld + seg;
+      A.rsrc0 = A.rsrc1 = make_rsrc(aa, ((int64_t)(g.dM - m0) * g.a_ld - seg) * 2);
+      A.ld = static_cast<uint32_t>(g.a_ld * 2); A.rows = g.dM - m0;
+      A.kmax0 = A.kmax1 = ne; A.nk0 = (ne + BK - 1) / BK;
     }
   };
   auto setupB = [&](const Tile& tl, BOp& B) __attribute__((always_inline)) {
@@ -557,10 +655,32 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       B.ptr0 = g.dhg_in + (int64_t)seg * f + n0; B.range0 = ((int64_t)ne * f - n0) * 2;
       B.ptr1 = g.dhu_in + (int64_t)seg * f + n0; B.range1 = B.range0;
       B.ld = f * 2; B.cols0 = B.cols1 = f - n0; B.kmax = ne;
-    } else {  // WGRAD_DOWN
+    } else if constexpr (MODE == WGRAD_DOWN) {
       B.ptr0 = g.dy + (int64_t)seg * d + n0; B.range0 = ((int64_t)ne * d - n0) * 2;
       B.ptr1 = B.ptr0 + 128; B.range1 = B.range0 - 256;
       B.ld = d * 2; B.cols0 = d - n0; B.cols1 = d - n0 - 128; B.kmax = ne;
+    } else if constexpr (MODE == RT_DW) {
+      // DL3 [T][E3p] = [hi | hi | lo]: sub-tile 0 from the first hi group,
+      // sub-tile 1 from the lo group, the same 128 experts
+      const uint16_t* r0 = g.db + seg * g.b_ld;
+      B.ptr0 = r0 + n0; B.range0 = ((int64_t)ne * g.b_ld - n0) * 2;
+      B.ptr1 = r0 + 2 * g.dE + n0; B.range1 = ((int64_t)ne * g.b_ld - 2 * g.dE - n0) * 2;
+      B.ld = static_cast<uint32_t>(g.b_ld * 2); B.cols0 = B.cols1 = g.dN - n0; B.kmax = ne;
+    } else if constexpr (MODE == VOC_DX) {
+      // W [H][ldw], K-contiguous rows h, the block's columns from bc0 + seg
+      const uint16_t* wb = g.db + (int64_t)n0 * g.b_ld + g.bc0 + seg;
+      B.rsrc0 = B.rsrc1 = make_rsrc(wb, ((int64_t)(g.dN - n0) * g.b_ld - g.bc0 - seg) * 2);
+      B.ld = static_cast<uint32_t>(g.b_ld * 2); B.rows = g.dN - n0;
+      B.kmax0 = B.kmax1 = ne; B.nk0 = (ne + BK - 1) / BK;
+    } else {
+      // N-contiguous dense B: RT_DX W3 [3E][d] (bc0 = 0); VOC_FWD/GRAD W
+      // [H][ldw] from column bc0 (the block); VOC_DW G [N][gp] (bc0 = 0)
+      const int64_t c0 = g.bc0;
+      const uint16_t* bb = g.db + c0 + seg * g.b_ld;
+      B.ptr0 = bb + n0; B.range0 = ((int64_t)ne * g.b_ld - c0 - n0) * 2;
+      B.ptr1 = B.ptr0 + 128; B.range1 = B.range0 - 256;
+      B.ld = static_cast<uint32_t>(g.b_ld * 2); B.cols0 = g.dN - n0; B.cols1 = g.dN - n0 - 128;
+      B.kmax = ne;
     }
   };
 
@@ -597,7 +717,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     // across the K loop, where they would be spilled)
     const int lane = opaque(threadIdx.x & 63);
     const int l32 = lane & 31, lh = lane >> 5;
-    const int mvalid = WGRAD ? ((MODE == WGRAD_GATE_UP ? d : f) - m0) : (ne - m0);
+    const int mvalid = DENSE   ? (g.dM - m0)
+                       : WGRAD ? ((MODE == WGRAD_GATE_UP ? d : f) - m0)
+                               : (ne - m0);
     typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
     typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
     typedef float f32x4v __attribute__((ext_vector_type(4)));
@@ -738,9 +860,160 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
           });
           fence();
         });
+      } else if constexpr (MODE == RT_DW) {
+        // fp32 partial dW_r of the batch: hi and lo sums of one expert column
+        // added, straight from the accumulators (4 consecutive columns per
+        // lane and row)
+        if (rb + l32 < mvalid) {
+          float* out = static_cast<float*>(g.dc) + (int64_t)e * g.c_bstride +
+                       (int64_t)(m0 + rb + l32) * g.c_ld;
+          static_for<4>([&](auto Q) {
+            constexpr int q = Q;
+            const int col = n0 + wn * 32 + 8 * q + 4 * lh;
+            const float v0 = acc[i][0][4 * q] + acc[i][1][4 * q];
+            const float v1 = acc[i][0][4 * q + 1] + acc[i][1][4 * q + 1];
+            const float v2 = acc[i][0][4 * q + 2] + acc[i][1][4 * q + 2];
+            const float v3 = acc[i][0][4 * q + 3] + acc[i][1][4 * q + 3];
+            if (col + 4 <= g.dN && (g.c_ld & 3) == 0) {
+              *reinterpret_cast<float4*>(out + col) = make_float4(v0, v1, v2, v3);
+            } else {
+              if (col < g.dN) out[col] = v0;
+              if (col + 1 < g.dN) out[col + 1] = v1;
+              if (col + 2 < g.dN) out[col + 2] = v2;
+              if (col + 3 < g.dN) out[col + 3] = v3;
+            }
+          });
+        }
+      } else if constexpr (MODE == VOC_FWD) {
+        // Per row, the (max, sum of exp(y - max)) of this wave's 64 block
+        // columns (lanes l and l + 32 hold 32 each), and the target's logit
+        // where this wave holds the target column.
+        const int rt = rb + l32;
+        const bool rok = rt < mvalid;
+        const int64_t row = (int64_t)m0 + rt;
+        const int cb = n0 + wn * 64;  // block column of the wave's first column
+        constexpr float NEG = -__builtin_huge_valf();
+        float mx = NEG;
+        static_for<2>([&](auto J) {
+          static_for<16>([&](auto R) {
+            constexpr int j = J, r = R;
+            const int c = cb + 32 * j + 8 * (r / 4) + 4 * lh + (r % 4);
+            if (c < g.dN) mx = fmaxf(mx, acc[i][j][r]);
+          });
+        });
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        float sm = 0.0f;
+        if (mx != NEG) {
+          static_for<2>([&](auto J) {
+            static_for<16>([&](auto R) {
+              constexpr int j = J, r = R;
+              const int c = cb + 32 * j + 8 * (r / 4) + 4 * lh + (r % 4);
+              if (c < g.dN) sm += __expf(acc[i][j][r] - mx);
+            });
+          });
+        }
+        sm += __shfl_xor(sm, 32, 64);
+        if (rok) {
+          const int ng = (g.dN + 63) >> 6;
+          if (lh == 0 && cb < g.dN)
+            reinterpret_cast<float2*>(g.dc)[row * ng + (cb >> 6)] = make_float2(mx, sm);
+          const int64_t tc = (int64_t)g.target[row] - g.v0 - cb;
+          if (tc >= 0 && tc < 64 && cb + tc < g.dN && ((tc >> 2) & 1) == lh) {
+            const int want = static_cast<int>(tc) & ~4;  // 32 j + 8 q + u
+            float val = 0.0f;
+            static_for<2>([&](auto J) {
+              static_for<16>([&](auto R) {
+                constexpr int j = J, r = R;
+                if (32 * j + 8 * (r / 4) + (r % 4) == want) val = acc[i][j][r];
+              });
+            });
+            g.yt[row] = val;
+          }
+        }
+      } else if constexpr (MODE == RT_DX || MODE == VOC_DX) {
+        // fp32 outputs through the patch, 16 rows at a time ([16][64] fp32,
+        // 256-byte rows, 16-byte chunk c of row r at c ^ r); each lane then
+        // finishes 8 consecutive outputs of one row:
+        //   RT_DX: dx = bf16([float(dx) +] v)   (one rounding)
+        //   VOC_DX: dxa[b] = v (first block) or dxa[b] + v
+        const int cg = lane & 7;
+        const int col = n0 + wn * 64 + 8 * cg;
+        static_for<2>([&](auto H) {
+          constexpr int h = H;
+          if ((l32 >> 4) == h) {
+            const int rr = l32 & 15;
+            static_for<2>([&](auto J) {
+              static_for<4>([&](auto Q) {
+                constexpr int j = J, q = Q;
+                const int c = 8 * j + 2 * q + lh;
+                put16(rr * 256 + ((c ^ rr) << 4),
+                      make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                  acc[i][j][4 * q + 3]));
+              });
+            });
+          }
+          fence();
+          static_for<2>([&](auto Tt) {
+            constexpr int t = Tt;
+            const int rr = 8 * t + (lane >> 3);
+            const float4 d0 = getf16(rr * 256 + (((2 * cg) ^ rr) << 4));
+            const float4 d1 = getf16(rr * 256 + (((2 * cg + 1) ^ rr) << 4));
+            const int rt = rb + 16 * h + rr;
+            if (rt < mvalid && col < g.dN) {
+              const int64_t row = (int64_t)m0 + rt;
+              float v[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+              if constexpr (MODE == RT_DX) {
+                uint4* o = reinterpret_cast<uint4*>(static_cast<uint16_t*>(g.dc) + row * g.c_ld + col);
+                if (g.flag) {
+                  const uint4 u = *o;
+                  const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+                  for (int q = 0; q < 4; ++q) {
+                    v[2 * q] = bf16_lo(w4[q]) + v[2 * q];
+                    v[2 * q + 1] = bf16_hi(w4[q]) + v[2 * q + 1];
+                  }
+                }
+                *o = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+              } else {
+                float4* o = reinterpret_cast<float4*>(static_cast<float*>(g.dc) +
+                                                      (int64_t)e * g.c_bstride + row * g.c_ld + col);
+                if (!g.flag) {
+                  const float4 a = o[0], b = o[1];
+                  v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+                  v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+                }
+                o[0] = make_float4(v[0], v[1], v[2], v[3]);
+                o[1] = make_float4(v[4], v[5], v[6], v[7]);
+              }
+            }
+          });
+          fence();
+        });
       } else {
         // one bf16 output, [32][64] bf16, 128-byte rows, 16-byte chunk c of
         // row r at c ^ ((r / 2) % 8)
+        if constexpr (MODE == VOC_GRAD) {
+          // the logit gradient of each value, G = dl ([v == t] - exp(y - lse)),
+          // 0 past the block's columns
+          const int rt = rb + l32;
+          float lse = 0.0f, dl = 0.0f;
+          int64_t tc = -1;
+          if (rt < mvalid) {
+            const int64_t row = (int64_t)m0 + rt;
+            lse = g.lse[row];
+            dl = g.dloss[row];
+            tc = (int64_t)g.target[row] - g.v0;
+          }
+          static_for<2>([&](auto J) {
+            static_for<16>([&](auto R) {
+              constexpr int j = J, r = R;
+              const int c = n0 + wn * 64 + 32 * j + 8 * (r / 4) + 4 * lh + (r % 4);
+              const float p = __expf(acc[i][j][r] - lse);
+              acc[i][j][r] = c < g.dN ? dl * ((c == tc ? 1.0f : 0.0f) - p) : 0.0f;
+            });
+          });
+        }
         static_for<2>([&](auto J) {
           static_for<4>([&](auto Q) {
             constexpr int j = J, q = Q;
@@ -754,11 +1027,16 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
           const int r = 8 * t + (lane >> 3), c = lane & 7;
           const uint4 v = unswap(get16(r * 128 + ((c ^ ((r >> 1) & 7)) << 4)), r);
           const int rt = rb + r, col = n0 + wn * 64 + 8 * c;
-          if (rt < mvalid && col < d) {
+          // column limit: d; the block's columns (VOC_DW); G's whole pitch,
+          // zeros past the block included (VOC_GRAD)
+          const int climit = MODE == VOC_GRAD ? static_cast<int>(g.c_ld) : DENSE ? g.dN : d;
+          if (rt < mvalid && col < climit) {
             uint16_t* out;
             if constexpr (MODE == FWD_DOWN) out = g.y + (int64_t)(seg + m0 + rt) * d;
             else if constexpr (MODE == DGRAD_GATE_UP) out = g.dx + (int64_t)(seg + m0 + rt) * d;
-            else out = g.dwd + e * wdf + (int64_t)(m0 + rt) * d;
+            else if constexpr (MODE == WGRAD_DOWN) out = g.dwd + e * wdf + (int64_t)(m0 + rt) * d;
+            else if constexpr (MODE == VOC_GRAD) out = static_cast<uint16_t*>(g.dc) + (int64_t)(m0 + rt) * g.c_ld;
+            else out = static_cast<uint16_t*>(g.dc) + (int64_t)(m0 + rt) * g.c_ld + g.cc0;  // VOC_DW
             *reinterpret_cast<uint4*>(out + col) = v;
           }
         });
@@ -1228,6 +1506,79 @@ hipError_t launch_ffn_bwd(const uint16_t* dy, const uint16_t* x_perm, const uint
       return e;
   }
   return hipSuccess;
+}
+
+// ------------------------------------------------------ dense products
+namespace {
+template <int MODE>
+hipError_t run_dense(GemmArgs& a, int kid, hipStream_t s) {
+  a.MT = static_cast<int>(ceil_div(a.dM, BM));
+  a.NT = static_cast<int>(ceil_div(a.dN, Traits<MODE>::DUAL ? BN / 2 : BN));
+  if (a.MT <= 0 || a.NT <= 0 || a.batches <= 0) return hipSuccess;
+  return run_gemm<MODE>(a, pgrid(), kid, s);
+}
+}  // namespace
+
+hipError_t launch_router_dw_mfma(const uint16_t* x, const uint16_t* dl3, int64_t T, int d, int E,
+                                 int64_t ld3, int64_t chunk, float* part, hipStream_t s) {
+  GemmArgs a{};
+  a.da = x; a.db = dl3; a.dc = part;
+  a.a_ld = d; a.b_ld = ld3; a.c_ld = E; a.c_bstride = static_cast<int64_t>(d) * E;
+  a.dM = d; a.dN = E; a.dK = static_cast<int>(T); a.dE = E;
+  a.kspan = static_cast<int>(chunk); a.batches = static_cast<int>(ceil_div(T, chunk));
+  return run_dense<RT_DW>(a, K_ROUTE_DW, s);
+}
+
+hipError_t launch_router_dx_mfma(const uint16_t* dl3, const uint16_t* w3, int64_t T, int d, int E,
+                                 int64_t ld3, int accumulate, uint16_t* dx, hipStream_t s) {
+  GemmArgs a{};
+  a.da = dl3; a.db = w3; a.dc = dx;
+  a.a_ld = ld3; a.b_ld = d; a.c_ld = d;
+  a.dM = static_cast<int>(T); a.dN = d; a.dK = 3 * E; a.kspan = 3 * E; a.batches = 1;
+  a.flag = accumulate;
+  return run_dense<RT_DX>(a, K_ROUTE_DX, s);
+}
+
+hipError_t launch_vocab_logits_mfma(const uint16_t* x, const uint16_t* w, int64_t ldw, int64_t bc0,
+                                    int64_t v0, int N, int H, int vb, const int32_t* target,
+                                    float* part, float* yt, hipStream_t s) {
+  GemmArgs a{};
+  a.da = x; a.db = w; a.dc = part; a.target = target; a.yt = yt;
+  a.a_ld = H; a.b_ld = ldw; a.bc0 = bc0; a.v0 = v0;
+  a.dM = N; a.dN = vb; a.dK = H; a.kspan = H; a.batches = 1;
+  return run_dense<VOC_FWD>(a, K_VOC_LOGITS, s);
+}
+
+hipError_t launch_vocab_grad_mfma(const uint16_t* x, const uint16_t* w, int64_t ldw, int64_t bc0,
+                                  int64_t v0, int N, int H, int vb, const int32_t* target,
+                                  const float* lse, const float* dloss, uint16_t* G, int64_t gp,
+                                  hipStream_t s) {
+  GemmArgs a{};
+  a.da = x; a.db = w; a.dc = G; a.target = target; a.lse = lse; a.dloss = dloss;
+  a.a_ld = H; a.b_ld = ldw; a.c_ld = gp; a.bc0 = bc0; a.v0 = v0;
+  a.dM = N; a.dN = vb; a.dK = H; a.kspan = H; a.batches = 1;
+  return run_dense<VOC_GRAD>(a, K_VOC_GRAD, s);
+}
+
+hipError_t launch_vocab_dx_mfma(const uint16_t* G, int64_t gp, const uint16_t* w, int64_t ldw,
+                                int64_t bc0, int N, int H, int vb, int kspan, int first,
+                                float* dxa, hipStream_t s) {
+  GemmArgs a{};
+  a.da = G; a.db = w; a.dc = dxa;
+  a.a_ld = gp; a.b_ld = ldw; a.c_ld = H; a.c_bstride = static_cast<int64_t>(N) * H; a.bc0 = bc0;
+  a.dM = N; a.dN = H; a.dK = vb; a.kspan = kspan;
+  a.batches = static_cast<int>(ceil_div(vb, kspan));
+  a.flag = first;
+  return run_dense<VOC_DX>(a, K_VOC_DX, s);
+}
+
+hipError_t launch_vocab_dw_mfma(const uint16_t* x, const uint16_t* G, int64_t gp, int N, int H,
+                                int vb, uint16_t* dw, int64_t ldd, int64_t cc0, hipStream_t s) {
+  GemmArgs a{};
+  a.da = x; a.db = G; a.dc = dw;
+  a.a_ld = H; a.b_ld = gp; a.c_ld = ldd; a.cc0 = cc0;
+  a.dM = H; a.dN = vb; a.dK = N; a.kspan = N; a.batches = 1;
+  return run_dense<VOC_DW>(a, K_VOC_DW, s);
 }
 
 }  // namespace moe

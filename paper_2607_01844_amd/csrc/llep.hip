@@ -165,13 +165,19 @@ __global__ __launch_bounds__(PT) void llep_offsets_kernel(const int32_t* __restr
 __global__ __launch_bounds__(256) void llep_window_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ offsets_all,
     const int32_t* __restrict__ dst_all, const int32_t* __restrict__ lo,
-    const int32_t* __restrict__ hi, const int32_t* __restrict__ offsets_r, int64_t A,
+    const int32_t* __restrict__ hi, const int32_t* __restrict__ offsets_r, int64_t A, int E,
     int32_t* __restrict__ row_src_r, int32_t* __restrict__ dst_r) {
   const int64_t a = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (a >= A) return;
   const int e = idx[a];
-  const int g = dst_all[a] - offsets_all[e];  // position among expert e's assignments
   int q = -1;
+  // an expert id outside [0, E) (caller garbage) or an assignment missing
+  // from the permutation is computed by no rank
+  if (static_cast<unsigned>(e) >= static_cast<unsigned>(E) || dst_all[a] < 0) {
+    dst_r[a] = -1;
+    return;
+  }
+  const int g = dst_all[a] - offsets_all[e];  // position among expert e's assignments
   if (g >= lo[e] && g < hi[e]) {
     q = offsets_r[e] + (g - lo[e]);
     if (q < offsets_r[e + 1]) row_src_r[q] = static_cast<int32_t>(a);
@@ -201,7 +207,7 @@ hipError_t launch_llep_dispatch(const uint16_t* x, const int32_t* idx, const int
   const int64_t A = T * k;
   if (A > 0)
     llep_window_kernel<<<static_cast<unsigned>(ceil_div(A, 256)), 256, 0, s>>>(
-        idx, offsets_all, dst_all, lo, hi, offsets_r, A, row_src_r, dst_r);
+        idx, offsets_all, dst_all, lo, hi, offsets_r, A, E, row_src_r, dst_r);
   prof_end(K_LLEP_WINDOW, s);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   if (A == 0) return hipSuccess;

@@ -177,6 +177,9 @@ __global__ __launch_bounds__(256) void route_logits_kernel(const uint16_t* __res
 // One wave per token: k rounds of a wave-wide arg-max over the not yet
 // chosen experts, ordered by (logit descending, index ascending).  Lane i
 // keeps slot i.  Gates: softmax over all E (renorm = 0) or over the chosen k.
+// A NaN logit ranks as -inf, so every round picks a valid expert (the
+// lowest free index when all free logits are -inf or NaN); gates of such a
+// token are unspecified.
 template <int NV>
 __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict__ logits,
                                                          int64_t T, int E, int k, int renorm,
@@ -192,7 +195,8 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   for (int i = 0; i < NV; ++i) {
     const int e = lane + 64 * i;
     if (e < E) {
-      v[i] = l[e];
+      const float le = l[e];
+      v[i] = le != le ? -__builtin_huge_valf() : le;
     } else {
       v[i] = -__builtin_huge_valf();
       taken |= 1u << i;

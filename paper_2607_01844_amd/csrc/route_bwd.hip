@@ -11,11 +11,12 @@
 // (|v - hi - lo| <= 2^-17 |v|), and the products are taken as
 //   dW_r = x^T (hi + lo)        (x is exactly bf16),
 //   dx_router = hi_d hi_w + hi_d lo_w + lo_d hi_w
-// with fp32 accumulation (rocBLAS products, atomics off; the token range of
-// dW_r is cut into chunks whose partial sums are added in chunk order).
+// with fp32 accumulation, on the library's grouped GEMM kernel (dense
+// modes); the token range of dW_r is cut into chunks whose partial sums are
+// added in chunk order.
 #include <algorithm>
 
-#include "blas.h"
+#include "common.h"
 
 namespace moe {
 namespace {
@@ -189,39 +190,42 @@ __global__ __launch_bounds__(256) void route_dw_reduce_kernel(const float* __res
   }
 }
 
-// hi / lo bf16 parts of fp32 values: dst row r gets, for each of its E
-// source values v, the parts in the column groups `order` names (0 = hi,
-// 1 = lo), so that one product over 3E columns sums the three cross terms.
+// hi / lo bf16 parts of fp32 values: hi = bf16(v), lo = bf16(v - hi).
 __device__ __forceinline__ void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
   hi = static_cast<uint16_t>(f32_to_bf16_bits(v));
   lo = static_cast<uint16_t>(f32_to_bf16_bits(v - bf16_to_f32(hi)));
 }
-// dl [T][E] -> b3 [T][3E] = [hi | hi | lo]
+// dl [T][E] -> dl3 [T][ld3] = [hi | hi | lo] (E columns each), zeros in
+// [3E, ld3): one product over the 3E columns against [hi; lo; hi] of W_r^T
+// sums the three cross terms, and the dW_r product reads the first hi group
+// and the lo group.
 __global__ __launch_bounds__(256) void route_split_dl_kernel(const float* __restrict__ dl,
-                                                             int64_t n, int E,
-                                                             uint16_t* __restrict__ b3) {
+                                                             int64_t T, int E, int ld3,
+                                                             uint16_t* __restrict__ dl3) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= n) return;
-  const int64_t t = i / E, e = i - t * E;
-  uint16_t hi, lo;
-  split_bf16(dl[i], hi, lo);
-  uint16_t* row = b3 + t * 3 * E;
-  row[e] = hi;
-  row[E + e] = hi;
-  row[2 * E + e] = lo;
+  if (i >= T * ld3) return;
+  const int64_t t = i / ld3;
+  const int c = static_cast<int>(i - t * ld3);
+  uint16_t out = 0;
+  if (c < 3 * E) {
+    const int grp = c / E, e = c - grp * E;
+    uint16_t hi, lo;
+    split_bf16(dl[t * E + e], hi, lo);
+    out = grp == 2 ? lo : hi;
+  }
+  dl3[i] = out;
 }
-// W_r [d][E] -> a3 [d][3E] = [hi | lo | hi]
-__global__ __launch_bounds__(256) void route_split_w_kernel(const float* __restrict__ w, int64_t n,
-                                                            int E, uint16_t* __restrict__ a3) {
+// W_r [d][E] -> w3 [3E][d] = [hi; lo; hi] of W_r^T
+__global__ __launch_bounds__(256) void route_split_w_kernel(const float* __restrict__ w, int d,
+                                                            int E, uint16_t* __restrict__ w3) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= n) return;
-  const int64_t j = i / E, e = i - j * E;
+  if (i >= static_cast<int64_t>(3) * E * d) return;
+  const int64_t r = i / d;
+  const int j = static_cast<int>(i - r * d);
+  const int grp = static_cast<int>(r / E), e = static_cast<int>(r - static_cast<int64_t>(grp) * E);
   uint16_t hi, lo;
-  split_bf16(w[i], hi, lo);
-  uint16_t* row = a3 + j * 3 * E;
-  row[e] = hi;
-  row[E + e] = lo;
-  row[2 * E + e] = hi;
+  split_bf16(w[static_cast<int64_t>(j) * E + e], hi, lo);
+  w3[i] = grp == 1 ? lo : hi;
 }
 // bpart[c][e] = sum over the tokens of chunk c, ascending, of dl[t][e]
 __global__ __launch_bounds__(256) void route_dbias_part_kernel(const float* __restrict__ dl,
@@ -317,26 +321,29 @@ namespace {
 bool route_bwd_mfma(int64_t T, int d, int E) {
   return T * static_cast<int64_t>(d) * E >= (int64_t{1} << 28);
 }
-// matrix-core path: token chunks of dW_r, so that the products have about
-// 512 output tiles of 256 x 256 between them
-int route_bwd_mfma_chunks(int64_t T, int d, int E) {
-  const int64_t tiles = ceil_div(d, 256) * ceil_div(E, 256);
-  return static_cast<int>(std::max<int64_t>(1, std::min(ceil_div(512, tiles), ceil_div(T, 256))));
+// matrix-core path: token chunks of dW_r (multiples of 64 tokens, at least
+// 512), so that the chunks' products have about 512 output tiles of 256 x
+// 256 between them
+int64_t route_bwd_mfma_chunk(int64_t T, int d, int E) {
+  const int64_t tiles = ceil_div(d, 256) * ceil_div(E, 128);
+  const int64_t S = std::max<int64_t>(1, std::min(ceil_div(512, tiles), ceil_div(T, 512)));
+  return static_cast<int64_t>(align_up(static_cast<size_t>(ceil_div(T, S)), 64));
 }
+int route_bwd_ld3(int E) { return static_cast<int>(align_up(static_cast<size_t>(3 * E), 8)); }
 }  // namespace
 
 size_t route_bwd_ws_bytes(int64_t T, int d, int E) {
   const bool mf = route_bwd_mfma(T, d, E);
-  const int S = mf ? route_bwd_mfma_chunks(T, d, E) : route_bwd_chunks(T, d, E);
+  const int S = mf ? static_cast<int>(ceil_div(T, route_bwd_mfma_chunk(T, d, E)))
+                   : route_bwd_chunks(T, d, E);
   size_t b = align_up(sizeof(float) * static_cast<size_t>(T) * E, 256);  // dlogits
   if (S > 1) {
     b += align_up(sizeof(float) * static_cast<size_t>(S) * d * E, 256);  // dW_r partials
     b += align_up(sizeof(float) * static_cast<size_t>(S) * E, 256);      // bias partials
   }
   if (mf) {
-    b += align_up(sizeof(uint16_t) * static_cast<size_t>(T) * 3 * E, 256);  // dl parts
-    b += align_up(sizeof(uint16_t) * static_cast<size_t>(d) * 3 * E, 256);  // W_r parts
-    b += kBlasWs;
+    b += align_up(sizeof(uint16_t) * static_cast<size_t>(T) * route_bwd_ld3(E), 256);  // dl parts
+    b += align_up(sizeof(uint16_t) * static_cast<size_t>(d) * 3 * E, 256);            // W_r parts
   }
   return b;
 }
@@ -347,76 +354,51 @@ namespace {
 hipError_t launch_route_bwd_mfma(const uint16_t* x, const float* w, int64_t T, int d, int E,
                                  const float* dl, float* dw, float* dbias, uint16_t* dx,
                                  int dx_accumulate, char* p, hipStream_t s) {
-  const int64_t chunk = ceil_div(T, route_bwd_mfma_chunks(T, d, E));
+  const int64_t chunk = route_bwd_mfma_chunk(T, d, E);
   const int S = static_cast<int>(ceil_div(T, chunk));  // chunks that hold tokens
   const int64_t nw = static_cast<int64_t>(d) * E;
-  const int E3 = 3 * E;
+  const int ld3 = route_bwd_ld3(E);
   float* part = dw;
-  float* bpart = nullptr;
+  float* bpart = dbias;
   if (S > 1) {
     part = reinterpret_cast<float*>(p);
     p += align_up(sizeof(float) * static_cast<size_t>(S) * nw, 256);
     bpart = reinterpret_cast<float*>(p);
     p += align_up(sizeof(float) * static_cast<size_t>(S) * E, 256);
   }
-  uint16_t* b3 = reinterpret_cast<uint16_t*>(p);
-  p += align_up(sizeof(uint16_t) * static_cast<size_t>(T) * E3, 256);
-  uint16_t* a3 = reinterpret_cast<uint16_t*>(p);
-  p += align_up(sizeof(uint16_t) * static_cast<size_t>(d) * E3, 256);
-  void* bws = p;
+  uint16_t* dl3 = reinterpret_cast<uint16_t*>(p);
+  p += align_up(sizeof(uint16_t) * static_cast<size_t>(T) * ld3, 256);
+  uint16_t* w3 = reinterpret_cast<uint16_t*>(p);
 
-  prof_begin(K_ROUTE_DW, s);
-  route_split_dl_kernel<<<static_cast<unsigned>(ceil_div(T * E, 256)), 256, 0, s>>>(dl, T * E, E,
-                                                                                   b3);
+  prof_begin(K_ROUTE_SPLIT, s);
+  route_split_dl_kernel<<<static_cast<unsigned>(ceil_div(T * ld3, 256)), 256, 0, s>>>(dl, T, E,
+                                                                                    ld3, dl3);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   if (dbias != nullptr) {
     route_dbias_part_kernel<<<dim3(static_cast<unsigned>(ceil_div(E, 256)),
                                    static_cast<unsigned>(S)),
-                              256, 0, s>>>(dl, T, E, chunk, S > 1 ? bpart : dbias);
+                              256, 0, s>>>(dl, T, E, chunk, bpart);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
-  {
-    BlasLease B(s, bws);
-    if (hipError_t e = B.status(); e != hipSuccess) return e;
-    // chunk c of tokens: part_c (col-major E x d = row-major [d][E]) =
-    // (hi + lo)_c (col-major E x chunk, columns of b3) x_c^T, full chunks in
-    // one batched product, the shorter last chunk on its own
-    const int64_t nfull = T / chunk, tail = T - nfull * chunk;
-    for (int pass = 0; pass < 2; ++pass) {
-      const uint16_t* A = b3 + (pass ? 2 * E : 0);
-      const float beta = pass ? 1.0f : 0.0f;
-      if (nfull > 0)
-        if (hipError_t e = gemm_bf16(B.handle(), false, true, E, d, static_cast<int>(chunk), A, E3,
-                                     chunk * E3, x, d, chunk * d, beta, part, false, E, nw,
-                                     static_cast<int>(nfull));
-            e != hipSuccess)
-          return e;
-      if (tail > 0)
-        if (hipError_t e = gemm_bf16(B.handle(), false, true, E, d, static_cast<int>(tail),
-                                     A + nfull * chunk * E3, E3, 0, x + nfull * chunk * d, d, 0,
-                                     beta, part + nfull * nw, false, E, 0);
-            e != hipSuccess)
-          return e;
-    }
-    if (S > 1) {
-      const int nb = dbias ? E : 0;
-      route_dw_reduce_kernel<<<static_cast<unsigned>(ceil_div(nw + nb, 256)), 256, 0, s>>>(
-          part, nw, S, dw, bpart, nb, dbias);
-      if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-    }
-    prof_end(K_ROUTE_DW, s);
-    if (dx == nullptr) return hipSuccess;
-    prof_begin(K_ROUTE_DX, s);
-    route_split_w_kernel<<<static_cast<unsigned>(ceil_div(nw, 256)), 256, 0, s>>>(w, nw, E, a3);
+  prof_end(K_ROUTE_SPLIT, s);
+  // part[c] = x_c^T (hi + lo)_c for every token chunk c
+  if (hipError_t e = launch_router_dw_mfma(x, dl3, T, d, E, ld3, chunk, part, s); e != hipSuccess)
+    return e;
+  if (S > 1) {
+    prof_begin(K_ROUTE_SPLIT, s);
+    const int nb = dbias ? E : 0;
+    route_dw_reduce_kernel<<<static_cast<unsigned>(ceil_div(nw + nb, 256)), 256, 0, s>>>(
+        part, nw, S, dw, bpart, nb, dbias);
+    prof_end(K_ROUTE_SPLIT, s);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-    // dx (col-major d x T) [+]= a3^T (d x 3E) b3 (3E x T), rounded to bf16 once
-    if (hipError_t e = gemm_bf16(B.handle(), true, false, d, static_cast<int>(T), E3, a3, E3, 0,
-                                 b3, E3, 0, dx_accumulate ? 1.0f : 0.0f, dx, true, d, 0);
-        e != hipSuccess)
-      return e;
-    prof_end(K_ROUTE_DX, s);
   }
-  return hipSuccess;
+  if (dx == nullptr) return hipSuccess;
+  prof_begin(K_ROUTE_SPLIT, s);
+  route_split_w_kernel<<<static_cast<unsigned>(ceil_div(3 * nw, 256)), 256, 0, s>>>(w, d, E, w3);
+  prof_end(K_ROUTE_SPLIT, s);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  // dx [+]= dl3 w3 over the 3E columns, rounded to bf16 once
+  return launch_router_dx_mfma(dl3, w3, T, d, E, ld3, dx_accumulate, dx, s);
 }
 }  // namespace
 

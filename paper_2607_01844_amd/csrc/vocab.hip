@@ -1,96 +1,74 @@
 // Blockwise vocabulary projection loss (the MoP paper's data-tensor-parallel
 // projection, Sec. 3.4 eq. voc-fwd-loss, on one device: P = 1, blocks of the
-// vocabulary instead of ranks).  Y = X W_voc is never materialised: the
-// forward walks the vocabulary in blocks of `vblock` columns, each block's
-// logits (fp32) feed a running max / sum of exponentials per token (an
-// online log-sum-exp, blocks merged in order, so the result is bitwise
-// reproducible); the backward recomputes each block's logits and turns them
-// into that block's logit gradients, from which it accumulates dX (fp32) and
-// writes the block's columns of dW.
-//
-// The three products per block are plain dense GEMMs and go to rocBLAS (bf16
-// operands, fp32 accumulation); everything between them is the kernels here.
-#include "blas.h"
+// vocabulary instead of ranks).  Y = X W_voc is never written anywhere:
+//  * forward, per block of `vblock` columns: one bf16 matrix-core product
+//    whose epilogue reduces each row's logits to a (max, sum exp(y - max))
+//    pair per 64 columns and picks up the target's logit; a one-wave-per-row
+//    kernel merges the block's pairs, in column order, into the row's running
+//    pair (blocks in order, so the result repeats bit for bit);
+//  * backward, per block: the product is recomputed and its epilogue turns
+//    each logit into the logit gradient G = dl ([v == t] - exp(y - lse)),
+//    rounded to bf16 (the only per-block buffer, N x vblock bf16); then
+//    dX += G W_block^T (fp32, the block's columns cut into K ranges that
+//    accumulate into separate fp32 slabs so the product fills the chip) and
+//    dW[:, block] = X^T G (bf16, each column written once).
+// All products run on the library's grouped GEMM kernel (dense modes).  When
+// V is not a multiple of 8 the rows of W and dW are not 16-byte aligned, so
+// each block of W is first copied into a padded buffer (and dW's block goes
+// through one on the way out).
+#include "common.h"
+
+#include <algorithm>
 
 namespace moe {
 namespace {
-
-constexpr int VT = 256;  // threads per block of the row kernels (one token row per block)
-constexpr int VU = 4;    // float4 loads in flight per thread
 
 // Merge of two (max, sum of exp(y - max)) pairs; an empty pair is (-inf, 0).
 __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
   const float mm = fmaxf(m, m2);
   if (mm == -__builtin_huge_valf()) return;  // both empty
-  s = s * expf(m - mm) + s2 * expf(m2 - mm);
+  s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
   m = mm;
 }
 
-// One block per token row n of a block of logits Y [N][pitch] (columns
-// [0, vb) valid, pitch a multiple of 4 so rows are 16-byte aligned): a single
-// pass keeps a running (max, sum) per thread over float4 groups, the block
-// combines the threads' pairs in a fixed tree, and thread 0 merges the
-// block's pair into the row's running (m, s) (blocks in order: bitwise
-// reproducible).  The target's logit is taken from the block that holds it.
-__global__ __launch_bounds__(VT) void voc_block_lse_kernel(const float* __restrict__ Y, int vb,
-                                                           int pitch, int64_t b0,
-                                                           const int32_t* __restrict__ target,
-                                                           float* __restrict__ m,
-                                                           float* __restrict__ s,
-                                                           float* __restrict__ yt, int first) {
-  __shared__ float sm[VT / 64], ss[VT / 64];
-  const int64_t n = blockIdx.x;
-  const float4* row = reinterpret_cast<const float4*>(Y + n * pitch);
-  const int nq = (vb + 3) >> 2;
-  constexpr float NEG = -__builtin_huge_valf();
-  float tm = NEG, ts = 0.0f;
-  for (int q0 = threadIdx.x; q0 < nq; q0 += VT * VU) {
-    float4 v[VU];
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int q = q0 + u * VT;
-      v[u] = q < nq ? row[q] : make_float4(NEG, NEG, NEG, NEG);
-    }
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int c = (q0 + u * VT) * 4;  // columns c..c+3; those >= vb are padding
-      const float a0 = v[u].x, a1 = c + 1 < vb ? v[u].y : NEG, a2 = c + 2 < vb ? v[u].z : NEG,
-                  a3 = c + 3 < vb ? v[u].w : NEG;
-      const float gm = fmaxf(fmaxf(a0, a1), fmaxf(a2, a3));
-      if (gm == NEG) continue;
-      if (gm > tm) {
-        ts *= expf(tm - gm);
-        tm = gm;
-      }
-      ts += (expf(a0 - tm) + expf(a1 - tm)) + (expf(a2 - tm) + expf(a3 - tm));
-    }
+// One wave per row n: the block's ng partial pairs part[n][0..ng) merged in
+// order (lane l takes groups l, l + 64, ... ascending, then a fixed xor
+// tree over the lanes), then merged into the row's running pair (m, s).
+__global__ __launch_bounds__(256) void voc_merge_kernel(const float2* __restrict__ part, int ng,
+                                                        int64_t N, float* __restrict__ m,
+                                                        float* __restrict__ s, int first) {
+  const int64_t n = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const float2* row = part + n * ng;
+  float tm = -__builtin_huge_valf(), ts = 0.0f;
+  for (int c = lane; c < ng; c += 64) {
+    const float2 p = row[c];
+    lse_merge(tm, ts, p.x, p.y);
   }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
+  for (int o = 1; o < 64; o <<= 1) {
     const float m2 = __shfl_xor(tm, o, 64), s2 = __shfl_xor(ts, o, 64);
-    lse_merge(tm, ts, m2, s2);
+    // both lanes of a pair compute the same merge in the same operand order
+    if (lane & o) {
+      float a = m2, b = s2;
+      lse_merge(a, b, tm, ts);
+      tm = a;
+      ts = b;
+    } else {
+      lse_merge(tm, ts, m2, s2);
+    }
   }
-  const int wv = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    sm[wv] = tm;
-    ss[wv] = ts;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float bm = sm[0], bs = ss[0];
-#pragma unroll
-    for (int k = 1; k < VT / 64; ++k) lse_merge(bm, bs, sm[k], ss[k]);
+  if (lane == 0) {
     if (first) {
-      m[n] = bm;
-      s[n] = bs;
+      m[n] = tm;
+      s[n] = ts;
     } else {
       float rm = m[n], rs = s[n];
-      lse_merge(rm, rs, bm, bs);
+      lse_merge(rm, rs, tm, ts);
       m[n] = rm;
       s[n] = rs;
     }
-    const int64_t t = target[n];
-    if (t >= b0 && t < b0 + vb) yt[n] = Y[n * pitch + (t - b0)];
   }
 }
 
@@ -107,46 +85,48 @@ __global__ __launch_bounds__(256) void voc_finalize_kernel(const float* __restri
   loss[n] = yt[n] - l;
 }
 
-// One block per token row: G[n][v] = bf16( dloss_n * ([b0 + v == t_n] -
-// exp(Y[n][v] - lse_n)) ), the gradient of loss_n with respect to this
-// block's logits, four columns per thread and store; padding columns
-// [vb, pitch) get zeros.
-__global__ __launch_bounds__(VT) void voc_grad_kernel(const float* __restrict__ Y, int vb,
-                                                      int pitch, int64_t b0,
-                                                      const int32_t* __restrict__ target,
-                                                      const float* __restrict__ lse,
-                                                      const float* __restrict__ dloss,
-                                                      uint16_t* __restrict__ G) {
-  const int64_t n = blockIdx.x;
-  const float4* row = reinterpret_cast<const float4*>(Y + n * pitch);
-  uint2* grow = reinterpret_cast<uint2*>(G + n * pitch);
-  const int nq = pitch >> 2;
-  const float l = lse[n], dl = dloss[n];
-  const int64_t tc = static_cast<int64_t>(target[n]) - b0;  // target column in this block
-  for (int q0 = threadIdx.x; q0 < nq; q0 += VT * VU) {
-    float4 v[VU];
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int q = q0 + u * VT;
-      v[u] = q < nq ? row[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int q = q0 + u * VT;
-      if (q >= nq) break;
-      const int c = q * 4;
-      float g[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        g[i] = c + i < vb ? dl * ((c + i == tc ? 1.0f : 0.0f) - expf(g[i] - l)) : 0.0f;
-      grow[q] = make_uint2(pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]));
-    }
+// dx[i] = bf16(sum over slabs b ascending of dxa[b][i]), 8 values per thread
+__global__ __launch_bounds__(256) void voc_dx_sum_kernel(const float* __restrict__ dxa, int slabs,
+                                                         int64_t n, uint16_t* __restrict__ dx) {
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (i >= n) return;  // n = N H is a multiple of 8
+  float v[8];
+  {
+    const float4 a = *reinterpret_cast<const float4*>(dxa + i);
+    const float4 b = *reinterpret_cast<const float4*>(dxa + i + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
   }
+  for (int sl = 1; sl < slabs; ++sl) {
+    const float* p = dxa + static_cast<int64_t>(sl) * n + i;
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w; v[4] += b.x; v[5] += b.y; v[6] += b.z;
+    v[7] += b.w;
+  }
+  *reinterpret_cast<uint4*>(dx + i) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                 pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
 }
 
-__global__ __launch_bounds__(256) void voc_fill_kernel(float* __restrict__ p, int64_t n) {
+// wst[h][c] = c < vb ? w[h][v0 + c] : 0 for c < vbp (padded copy of a block)
+__global__ __launch_bounds__(256) void voc_stage_kernel(const uint16_t* __restrict__ w, int64_t V,
+                                                        int64_t v0, int vb, int vbp, int H,
+                                                        uint16_t* __restrict__ wst) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i < n) p[i] = 0.0f;
+  if (i >= static_cast<int64_t>(H) * vbp) return;
+  const int64_t h = i / vbp;
+  const int c = static_cast<int>(i - h * vbp);
+  wst[i] = c < vb ? w[h * V + v0 + c] : uint16_t{0};
+}
+
+// dw[h][v0 + c] = dwst[h][c] for c < vb
+__global__ __launch_bounds__(256) void voc_unstage_kernel(const uint16_t* __restrict__ dwst,
+                                                          int vbp, int vb, int H, int64_t V,
+                                                          int64_t v0, uint16_t* __restrict__ dw) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(H) * vb) return;
+  const int64_t h = i / vb;
+  const int c = static_cast<int>(i - h * vb);
+  dw[h * V + v0 + c] = dwst[h * vbp + c];
 }
 
 __global__ __launch_bounds__(256) void voc_zero_bf16_kernel(uint16_t* __restrict__ p, int64_t n) {
@@ -154,58 +134,74 @@ __global__ __launch_bounds__(256) void voc_zero_bf16_kernel(uint16_t* __restrict
   if (i < n) p[i] = 0;
 }
 
-__global__ __launch_bounds__(256) void voc_to_bf16_kernel(const float* __restrict__ a, int64_t n,
-                                                          uint16_t* __restrict__ b) {
-  const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 2;
-  if (i >= n) return;  // n is even (H is a multiple of 8)
-  *reinterpret_cast<uint32_t*>(b + i) = pack_bf16x2(a[i], a[i + 1]);
+bool staged(int64_t V) { return (V % 8) != 0; }
+
+// K ranges of the dX product: enough (row tile x column tile x range) work
+// items for about two per compute unit of a 256-CU device, each range at
+// least 512 columns (a multiple of 64)
+int64_t dx_kspan(int64_t N, int H, int64_t vblock) {
+  const int64_t tiles = std::max<int64_t>(1, ceil_div(N, 256) * ceil_div(H, 256));
+  int64_t S = std::min<int64_t>(8, std::max<int64_t>(1, ceil_div(512, tiles)));
+  S = std::max<int64_t>(1, std::min<int64_t>(S, vblock / 512));
+  return align_up(static_cast<size_t>(ceil_div(vblock, S)), 64);
 }
 
 }  // namespace
 
-size_t vocab_fwd_ws_bytes(int64_t N, int64_t vblock) {
-  return align_up(sizeof(float) * static_cast<size_t>(N) * vblock, 256) +
-         3 * align_up(sizeof(float) * static_cast<size_t>(N), 256) + kBlasWs + 256;
+size_t vocab_fwd_ws_bytes(int64_t N, int H, int64_t V, int64_t vblock) {
+  const int64_t vb = std::min(vblock, V);
+  size_t b = align_up(sizeof(float) * 2 * static_cast<size_t>(N) * ceil_div(vb, 64), 256);  // pairs
+  b += 3 * align_up(sizeof(float) * static_cast<size_t>(N), 256);  // running max, sum; target logit
+  if (staged(V)) b += align_up(sizeof(uint16_t) * static_cast<size_t>(H) * align_up(vb, 8), 256);
+  return b + 256;
 }
 
-size_t vocab_bwd_ws_bytes(int64_t N, int H, int64_t vblock) {
-  return align_up(sizeof(float) * static_cast<size_t>(N) * vblock, 256) +
-         align_up(sizeof(uint16_t) * static_cast<size_t>(N) * vblock, 256) +
-         align_up(sizeof(float) * static_cast<size_t>(N) * H, 256) + kBlasWs + 256;
+size_t vocab_bwd_ws_bytes(int64_t N, int H, int64_t V, int64_t vblock) {
+  const int64_t vb = std::min(vblock, V);
+  const int64_t vbp = align_up(vb, 8);
+  const int64_t slabs = ceil_div(vb, dx_kspan(N, H, vblock));
+  size_t b = align_up(sizeof(uint16_t) * static_cast<size_t>(N) * vbp, 256);            // G
+  b += align_up(sizeof(float) * static_cast<size_t>(slabs) * N * H, 256);                // dX slabs
+  if (staged(V)) b += 2 * align_up(sizeof(uint16_t) * static_cast<size_t>(H) * vbp, 256);  // W, dW
+  return b + 256;
 }
 
-// Row-major [r][c] with pitch ld is column-major c x r with the same pitch,
-// which is how every product below is handed to rocBLAS.  A block's logits
-// and logit gradients use a row pitch of vb rounded up to 8 columns, so
-// every row starts 16-byte aligned; the padding columns are never read by
-// the products.
 hipError_t launch_vocab_fwd(const uint16_t* x, const uint16_t* w, const int32_t* target,
                             int64_t N, int H, int64_t V, int64_t vblock, float* loss, float* lse,
                             void* ws, hipStream_t s) {
   if (N == 0) return hipSuccess;
+  const int64_t vbmax = std::min(vblock, V);
   char* p = static_cast<char*>(ws);
-  float* Y = reinterpret_cast<float*>(p);
-  p += align_up(sizeof(float) * static_cast<size_t>(N) * vblock, 256);
+  float* part = reinterpret_cast<float*>(p);
+  p += align_up(sizeof(float) * 2 * static_cast<size_t>(N) * ceil_div(vbmax, 64), 256);
   float* m = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * static_cast<size_t>(N), 256);
   float* sm = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * static_cast<size_t>(N), 256);
   float* yt = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * static_cast<size_t>(N), 256);
-  void* bws = p;
-  BlasLease B(s, bws);
-  if (hipError_t e = B.status(); e != hipSuccess) return e;
-  const unsigned gr = static_cast<unsigned>(N);
+  uint16_t* wst = staged(V) ? reinterpret_cast<uint16_t*>(p) : nullptr;
+  const int n = static_cast<int>(N);
   for (int64_t b0 = 0; b0 < V; b0 += vblock) {
     const int vb = static_cast<int>(std::min<int64_t>(vblock, V - b0));
-    const int pitch = static_cast<int>(align_up(vb, 8));
-    // Y[N][vb] = X[N][H] W[H][b0 : b0 + vb]
-    if (hipError_t e = gemm_bf16(B.handle(), false, false, vb, static_cast<int>(N), H, w + b0,
-                                 static_cast<int>(V), 0, x, H, 0, 0.0f, Y, false, pitch, 0);
+    const uint16_t* wb = w;
+    int64_t ldw = V, bc0 = b0;
+    if (wst != nullptr) {
+      const int vbp = static_cast<int>(align_up(vb, 8));
+      voc_stage_kernel<<<static_cast<unsigned>(ceil_div(static_cast<int64_t>(H) * vbp, 256)), 256,
+                         0, s>>>(w, V, b0, vb, vbp, H, wst);
+      if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+      wb = wst;
+      ldw = vbp;
+      bc0 = 0;
+    }
+    if (hipError_t e = launch_vocab_logits_mfma(x, wb, ldw, bc0, b0, n, H, vb, target, part, yt, s);
         e != hipSuccess)
       return e;
     prof_begin(K_VOC_LSE, s);
-    voc_block_lse_kernel<<<gr, VT, 0, s>>>(Y, vb, pitch, b0, target, m, sm, yt, b0 == 0);
+    voc_merge_kernel<<<static_cast<unsigned>(ceil_div(N, 4)), 256, 0, s>>>(
+        reinterpret_cast<const float2*>(part), static_cast<int>(ceil_div(vb, 64)), N, m, sm,
+        b0 == 0);
     prof_end(K_VOC_LSE, s);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
@@ -217,50 +213,63 @@ hipError_t launch_vocab_fwd(const uint16_t* x, const uint16_t* w, const int32_t*
 hipError_t launch_vocab_bwd(const uint16_t* x, const uint16_t* w, const int32_t* target,
                             const float* lse, const float* dloss, int64_t N, int H, int64_t V,
                             int64_t vblock, uint16_t* dx, uint16_t* dw, void* ws, hipStream_t s) {
-  if (N == 0) {  // no tokens: both gradients are exact zeros
+  if (N == 0) {  // no tokens: the weight gradient is exact zeros (dx is empty)
     const int64_t nw = static_cast<int64_t>(H) * V;
     voc_zero_bf16_kernel<<<static_cast<unsigned>(ceil_div(nw, 256)), 256, 0, s>>>(dw, nw);
     return hipGetLastError();
   }
+  const int64_t vbmax = std::min(vblock, V);
+  const int64_t vbpmax = align_up(vbmax, 8);
+  const int kspan = static_cast<int>(dx_kspan(N, H, vblock));
+  const int slabs = static_cast<int>(ceil_div(vbmax, kspan));  // the first block fills them all
   char* p = static_cast<char*>(ws);
-  float* Y = reinterpret_cast<float*>(p);
-  p += align_up(sizeof(float) * static_cast<size_t>(N) * vblock, 256);
   uint16_t* G = reinterpret_cast<uint16_t*>(p);
-  p += align_up(sizeof(uint16_t) * static_cast<size_t>(N) * vblock, 256);
+  p += align_up(sizeof(uint16_t) * static_cast<size_t>(N) * vbpmax, 256);
   float* dxa = reinterpret_cast<float*>(p);
-  p += align_up(sizeof(float) * static_cast<size_t>(N) * H, 256);
-  void* bws = p;
-  BlasLease B(s, bws);
-  if (hipError_t e = B.status(); e != hipSuccess) return e;
-  const int64_t nx = N * H;
-  voc_fill_kernel<<<static_cast<unsigned>(ceil_div(nx, 256)), 256, 0, s>>>(dxa, nx);
-  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-  const int n = static_cast<int>(N), ldw = static_cast<int>(V);
+  p += align_up(sizeof(float) * static_cast<size_t>(slabs) * N * H, 256);
+  uint16_t* wst = nullptr;
+  uint16_t* dwst = nullptr;
+  if (staged(V)) {
+    wst = reinterpret_cast<uint16_t*>(p);
+    p += align_up(sizeof(uint16_t) * static_cast<size_t>(H) * vbpmax, 256);
+    dwst = reinterpret_cast<uint16_t*>(p);
+  }
+  const int n = static_cast<int>(N);
   for (int64_t b0 = 0; b0 < V; b0 += vblock) {
     const int vb = static_cast<int>(std::min<int64_t>(vblock, V - b0));
-    const int pitch = static_cast<int>(align_up(vb, 8));
-    // Y[N][vb] = X W[:, b0 : b0 + vb]   (recomputed)
-    if (hipError_t e = gemm_bf16(B.handle(), false, false, vb, n, H, w + b0, ldw, 0, x, H, 0, 0.0f,
-                                 Y, false, pitch, 0);
+    const int64_t gp = align_up(vb, 8);
+    const uint16_t* wb = w;
+    int64_t ldw = V, bc0 = b0;
+    uint16_t* dwb = dw;
+    int64_t ldd = V, cc0 = b0;
+    if (wst != nullptr) {
+      voc_stage_kernel<<<static_cast<unsigned>(ceil_div(static_cast<int64_t>(H) * gp, 256)), 256,
+                         0, s>>>(w, V, b0, vb, static_cast<int>(gp), H, wst);
+      if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+      wb = wst;
+      ldw = gp;
+      bc0 = 0;
+      dwb = dwst;
+      ldd = gp;
+      cc0 = 0;
+    }
+    if (hipError_t e = launch_vocab_grad_mfma(x, wb, ldw, bc0, b0, n, H, vb, target, lse, dloss, G,
+                                              gp, s);
         e != hipSuccess)
       return e;
-    prof_begin(K_VOC_GRAD, s);
-    voc_grad_kernel<<<static_cast<unsigned>(N), VT, 0, s>>>(Y, vb, pitch, b0, target, lse, dloss,
-                                                           G);
-    prof_end(K_VOC_GRAD, s);
-    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-    // dX[N][H] += G[N][vb] W[:, b0 : b0 + vb]^T
-    if (hipError_t e = gemm_bf16(B.handle(), true, false, H, n, vb, w + b0, ldw, 0, G, pitch, 0,
-                                 1.0f, dxa, false, H, 0);
+    if (hipError_t e = launch_vocab_dx_mfma(G, gp, wb, ldw, bc0, n, H, vb, kspan, b0 == 0, dxa, s);
         e != hipSuccess)
       return e;
-    // dW[:, b0 : b0 + vb] = X^T G
-    if (hipError_t e = gemm_bf16(B.handle(), false, true, vb, H, n, G, pitch, 0, x, H, 0, 0.0f,
-                                 dw + b0, true, ldw, 0);
-        e != hipSuccess)
+    if (hipError_t e = launch_vocab_dw_mfma(x, G, gp, n, H, vb, dwb, ldd, cc0, s); e != hipSuccess)
       return e;
+    if (dwst != nullptr) {
+      voc_unstage_kernel<<<static_cast<unsigned>(ceil_div(static_cast<int64_t>(H) * vb, 256)), 256,
+                           0, s>>>(dwst, static_cast<int>(gp), vb, H, V, b0, dw);
+      if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    }
   }
-  voc_to_bf16_kernel<<<static_cast<unsigned>(ceil_div(nx / 2, 256)), 256, 0, s>>>(dxa, nx, dx);
+  const int64_t nx = N * H;
+  voc_dx_sum_kernel<<<static_cast<unsigned>(ceil_div(nx / 8, 256)), 256, 0, s>>>(dxa, slabs, nx, dx);
   return hipGetLastError();
 }
 

@@ -119,13 +119,21 @@ def _need(t, dtype, name, dim=None):
 
 
 _ws_cache: dict = {}
+_ws_retired: list = []
 
 
 def workspace(nbytes: int, device, tag: str) -> torch.Tensor:
-    """A cached device scratch buffer of at least nbytes (per device and tag)."""
-    key = (str(device), tag)
+    """A cached device scratch buffer of at least nbytes, one per (device,
+    current stream, tag): calls on one stream are ordered, calls on different
+    streams get different buffers.  A buffer replaced by a larger one is
+    kept alive until the process ends, so a HIP graph captured with it never
+    replays into freed memory (capture with the sizes it will replay)."""
+    stream = torch.cuda.current_stream(device).cuda_stream
+    key = (str(device), stream, tag)
     buf = _ws_cache.get(key)
     if buf is None or buf.numel() < nbytes:
+        if buf is not None:
+            _ws_retired.append(buf)
         buf = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
         _ws_cache[key] = buf
     return buf

@@ -155,18 +155,26 @@ def test_workspace_too_small_rejected(lib):
     assert lib.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
 
 
-def test_vocab_workspace_is_one_block_of_logits():
-    """The vocabulary loss keeps one N x vblock block of logits (fp32, plus
-    its bf16 gradient) and an fp32 dX accumulator, never N x V."""
+def test_vocab_workspace_is_one_block_of_gradients():
+    """The vocabulary loss keeps no logits at all: per block, one N x vblock
+    bf16 block of logit gradients, (max, sum) pairs per 64 columns, and a few
+    fp32 dX slabs (the K ranges of the dX product); never N x V, and not even
+    an fp32 N x vblock block of logits."""
     from paper_2607_01844_amd import moe
     L = moe.lib
-    n1, n2 = ctypes.c_size_t(), ctypes.c_size_t()
-    assert L.moe_vocab_loss_workspace_bytes(4096, 2048, 200000, 16384, ctypes.byref(n1)) == 0
-    assert L.moe_vocab_loss_workspace_bytes(4096, 2048, 400000, 16384, ctypes.byref(n2)) == 0
+    N, H, vb = 4096, 2048, 16384
+    n1, n2, n3 = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.moe_vocab_loss_workspace_bytes(N, H, 200000, vb, ctypes.byref(n1)) == 0
+    assert L.moe_vocab_loss_workspace_bytes(N, H, 400000, vb, ctypes.byref(n2)) == 0
     assert n1.value == n2.value  # independent of V
-    base = 4096 * 16384 * 6 + 4096 * 2048 * 4
-    assert base <= n1.value <= base + (33 << 20)
-    assert n1.value < 4096 * 200000 * 4 // 4
+    g_block = N * vb * 2
+    assert g_block <= n1.value <= g_block + 8 * N * H * 4 + (1 << 20)
+    assert n1.value < g_block + N * vb * 4  # no fp32 block of logits besides G
+    assert n1.value < N * 200000 * 4 // 4
+    # a vocabulary that is not a multiple of 8 adds padded copies of one
+    # block of W and of dW (H x vblock bf16 each)
+    assert L.moe_vocab_loss_workspace_bytes(N, H, 200001, vb, ctypes.byref(n3)) == 0
+    assert n3.value - n1.value <= 2 * H * vb * 2 + 4096
 
 
 def test_chunked_workspace_depends_on_chunk_only(lib):

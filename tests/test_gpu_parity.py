@@ -138,6 +138,27 @@ def test_exact_ties_lowest_index():
             assert row.index(1) < row.index(4)
 
 
+def test_nan_logits_rank_last():
+    """NaN logits (here from a NaN router bias) rank as -inf: every index
+    lies in [0, E) and equals the oracle's selection bit for bit."""
+    import oracle
+    moe = _moe()
+    wl = W.Workload("nan", T=300, d=64, E=70, k=6, f=32)
+    bias = np.zeros(wl.E, np.float32)
+    bias[[0, 3, 64, 65]] = np.nan
+    inp = make(wl, bias=bias)
+    lg = torch.empty((wl.T, wl.E), dtype=torch.float32, device="cuda")
+    idx, _ = moe.moe_route(inp["x"], inp["w_router"], inp["router_bias"], wl.k, 0, logits=lg)
+    torch.cuda.synchronize()
+    got = idx.cpu().numpy()
+    assert np.all((got >= 0) & (got < wl.E))
+    h = P.host_inputs(inp)
+    ref_lg = oracle.logits(h["x"], h["w_r"], h["bias"], "f32")
+    ref_idx, _ = oracle.topk(ref_lg, wl.k, 0)
+    assert np.array_equal(got, ref_idx)
+    assert not np.isin(got, [0, 3, 64, 65]).any()  # the NaN experts are never chosen
+
+
 def test_zero_tokens():
     moe = _moe()
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")

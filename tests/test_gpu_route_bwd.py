@@ -77,6 +77,8 @@ SMALL = [
     # shorter last token chunk and d not a multiple of 256 in the second
     ("mfma", 2048, 1024, 128, 6, 0, True, True, True, True),
     ("mfma_ragged", 2100, 1032, 128, 4, 1, False, False, True, False),
+    # E not a multiple of 8 (padded columns of the split logit gradients)
+    ("mfma_E100", 2624, 1024, 100, 4, 0, True, True, True, True),
 ]
 
 

@@ -60,6 +60,10 @@ SMALL = [
     ("t1", 1, 8, 9, [8, 16]),
     ("V1", 9, 16, 1, [8]),
     ("wide_H", 70, 520, 333, [64, 200]),
+    # the dX product in 2 and 4 K ranges over several blocks, aligned and
+    # not (V % 8 != 0: W and dW go through padded block copies)
+    ("split_k", 300, 136, 3000, [1024, 2048]),
+    ("split_k_staged", 300, 136, 3001, [1024]),
 ]
 
 

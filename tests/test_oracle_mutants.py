@@ -23,8 +23,10 @@ MUTANTS = {
     "gate_up_weights_swapped": (
         "      hg[n] += xj * widen<R>(g[n]);\n      hu[n] += xj * widen<R>(u[n]);",
         "      hg[n] += xj * widen<R>(u[n]);\n      hu[n] += xj * widen<R>(g[n]);"),
-    "ties_prefer_higher_index": ("return l[a] > l[b]; });",
-                                 "return l[a] > l[b] || (l[a] == l[b] && a > b); });"),
+    "ties_prefer_higher_index": ("return key(a) > key(b); });",
+                                 "return key(a) > key(b) || (key(a) == key(b) && a > b); });"),
+    "nan_ranks_first": ("return std::isnan(l[e]) ? -std::numeric_limits<L>::infinity() : l[e];",
+                        "return std::isnan(l[e]) ? std::numeric_limits<L>::infinity() : l[e];"),
     "bias_sign": ("if (bias) acc = acc + bias[e];", "if (bias) acc = acc - bias[e];"),
     "dw_down_wrong_operand": ("const R am = a[p * f + m];", "const R am = dhg[p * f + m];"),
     "dy_perm_without_gate": ("dy_perm[p * d + c] = g * dv;", "dy_perm[p * d + c] = dv;"),

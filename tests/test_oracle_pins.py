@@ -92,6 +92,31 @@ def test_topk_matches_lexsort(orc):
     assert list(idx[1][:4]) == [0, 1, 2, 3]      # -0 == +0 is a tie
 
 
+def test_topk_nan_ranks_as_minus_inf(orc):
+    """NaN logits rank as -inf (ties by index): the selection always names
+    valid experts.  Brute force: lexsort with NaN replaced by -inf."""
+    E = 12
+    lg = np.random.default_rng(2).standard_normal((5, E)).astype(np.float32)
+    lg[0, :] = np.nan                       # all NaN: the lowest indices
+    lg[1, [0, 5]] = np.nan                  # NaN where the largest would be
+    lg[1, 5] = np.nan
+    lg[2, :] = -np.inf
+    lg[2, [3, 7]] = np.nan                  # NaN and -inf tie
+    lg[3, 4] = np.inf
+    lg[3, 2] = np.nan
+    for k in (1, 4, E):
+        idx, _ = orc.topk(lg, k)
+        assert np.all((idx >= 0) & (idx < E))
+        for t in range(lg.shape[0]):
+            key = np.where(np.isnan(lg[t]), -np.inf, lg[t]).astype(np.float64)
+            ref = np.lexsort((np.arange(E), -key))[:k]
+            assert np.array_equal(idx[t], ref), (t, k)
+    idx, _ = orc.topk(lg, 4)
+    assert list(idx[0]) == [0, 1, 2, 3]
+    assert list(idx[2]) == [0, 1, 2, 3]
+    assert idx[3][0] == 4
+
+
 def test_gates_closed_form(orc):
     rng = np.random.default_rng(7)
     T, E, k = 50, 16, 4
