@@ -54,6 +54,7 @@ extern "C" {
 #define MOE_MAX_E 1024
 #define MOE_MAX_DIM 262144
 #define MOE_LLEP_MAX_RANKS 64
+#define MOE_PERMUTE_NOALLOC_MAX_BYTES 8388608
 
 typedef uint16_t moe_bf16;
 
@@ -156,6 +157,24 @@ int moe_permute(const moe_bf16* x, const int32_t* topk_idx, int64_t T, int d, in
                 int expert_begin, int num_local, int32_t* expert_offsets,
                 int32_t* counts_global, int32_t* row_src, int32_t* dst, moe_bf16* x_perm,
                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* moe_permute_noalloc: moe_permute for callers that cannot allocate device
+ * memory or pass a workspace (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, results and
+ * errors as moe_permute, minus the workspace: the call uses a static device
+ * array of MOE_PERMUTE_NOALLOC_MAX_BYTES (8 MiB) that the library holds on
+ * every GPU it runs on until the process ends, and calls no hipMalloc or
+ * hipFree.  Sizes whose moe_permute_workspace_bytes() exceed that limit
+ * (about T*k/4096 * (2*num_local + E) * 4 bytes; e.g. T*k = 2^19 with
+ * E = 128 needs 0.2 MiB) return MOE_ERR_UNSUPPORTED.  Every call on one GPU
+ * shares that GPU's array and leaves its contents behind: calls that
+ * overlap on one GPU (different streams, or concurrent host threads)
+ * race, so callers keep them ordered on one stream.
+ */
+int moe_permute_noalloc(const moe_bf16* x, const int32_t* topk_idx, int64_t T, int d, int E,
+                        int k, int expert_begin, int num_local, int32_t* expert_offsets,
+                        int32_t* counts_global, int32_t* row_src, int32_t* dst,
+                        moe_bf16* x_perm, void* stream);
 
 /* ----------------------------------------------------- grouped SwiGLU FFN
  * Expert feed-forward on the permuted rows (Sec. 3.1: Theta_exp = Theta(LEHI)

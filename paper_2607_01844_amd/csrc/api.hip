@@ -249,6 +249,31 @@ MOE_API int moe_permute(const moe_bf16* x, const int32_t* topk_idx, int64_t T, i
                     fn);
 }
 
+MOE_API int moe_permute_noalloc(const moe_bf16* x, const int32_t* topk_idx, int64_t T, int d,
+                                int E, int k, int expert_begin, int num_local,
+                                int32_t* expert_offsets, int32_t* counts_global,
+                                int32_t* row_src, int32_t* dst, moe_bf16* x_perm, void* stream) {
+  const char* fn = "moe_permute_noalloc";
+  if (int r = check_tk(fn, T, E, k)) return r;
+  if (int r = check_dim(fn, d, "d")) return r;
+  CHECK(num_local >= 1, "num_local < 1");
+  CHECK(expert_begin >= 0 && static_cast<int64_t>(expert_begin) + num_local <= E,
+        "expert range outside [0, E)");
+  REQ(expert_offsets);
+  OPT(counts_global);
+  if (T > 0) {
+    REQ(x); REQ(topk_idx); REQ(row_src); REQ(dst); REQ(x_perm);
+  }
+  if (moe::permute_ws_bytes(T, E, k, num_local) > MOE_PERMUTE_NOALLOC_MAX_BYTES)
+    return fail(MOE_ERR_UNSUPPORTED, fn,
+                "the scratch this size needs (moe_permute_workspace_bytes) exceeds "
+                "MOE_PERMUTE_NOALLOC_MAX_BYTES; use moe_permute with a workspace");
+  return hip_status(moe::launch_permute_noalloc(x, topk_idx, T, d, E, k, expert_begin, num_local,
+                                                expert_offsets, counts_global, row_src, dst,
+                                                x_perm, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 // ----------------------------------------------------- grouped SwiGLU FFN
 MOE_API int moe_grouped_swiglu_workspace_bytes(int64_t cap, int num_local, int d, int f,
                                                unsigned flags, size_t* bytes) {

@@ -138,6 +138,13 @@ hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int 
                           hipStream_t s);
 hipError_t launch_gather(const uint16_t* x, const int32_t* dst, int64_t T, int d, int k,
                          uint16_t* x_perm, hipStream_t s);
+// launch_permute with the library's static scratch as the workspace
+// (permute_ws_bytes(T, E, k, E_loc) <= MOE_PERMUTE_NOALLOC_MAX_BYTES, checked
+// by the caller)
+hipError_t launch_permute_noalloc(const uint16_t* x, const int32_t* idx, int64_t T, int d, int E,
+                                  int k, int e_begin, int E_loc, int32_t* offsets,
+                                  int32_t* counts_global, int32_t* row_src, int32_t* dst,
+                                  uint16_t* x_perm, hipStream_t s);
 hipError_t launch_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* lo,
                             int32_t* hi, int32_t* load, int32_t* n_ship, hipStream_t s);
 hipError_t launch_llep_dispatch(const uint16_t* x, const int32_t* idx, const int32_t* offsets_all,

@@ -11,9 +11,22 @@
 //      lower lanes).  Positions never depend on atomic return order.
 //   4. gather: one wave per token reads x[t] once and writes it to each of
 //      the token's local rows.
+#include <mutex>
+
 #include "common.h"
 
 namespace moe {
+
+// Scratch of the allocation-free permutation (moe_permute_noalloc): the
+// per-block expert counts and bases, in a static device array that every
+// GPU the library runs on holds until the process ends.  In host code the
+// array's name is only a host-side stand-in, never a device address: the
+// device address comes from hipGetSymbolAddress, looked up once per device
+// with that device current.  Every call on one GPU shares that GPU's copy,
+// so calls that overlap on one GPU (different streams) race.  The kernels
+// write every scratch word they read, so nothing is cleared between calls.
+static __device__ __align__(256) char scratch[MOE_PERMUTE_NOALLOC_MAX_BYTES];
+
 namespace {
 
 constexpr int CH = 4096;          // assignments per count/rank block
@@ -249,6 +262,38 @@ hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int 
                                                                            x_perm);
   prof_end(K_PERM_GATHER, s);
   return hipGetLastError();
+}
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+
+// the current device's address of `scratch` (looked up on first use)
+hipError_t scratch_address(void** out) {
+  int dev = -1;
+  if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)); e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_permute_noalloc(const uint16_t* x, const int32_t* idx, int64_t T, int d, int E,
+                                  int k, int e_begin, int E_loc, int32_t* offsets,
+                                  int32_t* counts_global, int32_t* row_src, int32_t* dst,
+                                  uint16_t* x_perm, hipStream_t s) {
+  void* ws = nullptr;
+  if (hipError_t e = scratch_address(&ws); e != hipSuccess) return e;
+  return launch_permute(x, idx, T, d, E, k, e_begin, E_loc, offsets, counts_global, row_src, dst,
+                        x_perm, ws, s);
 }
 
 hipError_t launch_gather(const uint16_t* x, const int32_t* dst, int64_t T, int d, int k,

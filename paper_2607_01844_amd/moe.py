@@ -22,12 +22,13 @@ MOE_BWD_WGRAD = 2
 MOE_MAX_K = 16
 MOE_MAX_E = 1024
 MOE_MAX_DIM = 262144
+MOE_PERMUTE_NOALLOC_MAX_BYTES = 8 << 20
 
 C_SYMBOLS = (
     "moe_abi_version", "moe_status_string", "moe_last_error",
     "moe_route_workspace_bytes", "moe_route",
     "moe_route_bwd_workspace_bytes", "moe_route_bwd",
-    "moe_permute_workspace_bytes", "moe_permute",
+    "moe_permute_workspace_bytes", "moe_permute", "moe_permute_noalloc",
     "moe_grouped_swiglu_workspace_bytes", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
     "moe_combine", "moe_combine_bwd",
     "moe_ffn_fwd_chunked_workspace_bytes", "moe_ffn_fwd_chunked",
@@ -60,6 +61,7 @@ def _load():
         "moe_route_bwd": ([P, P, P, P, P, P, I64, I, I, I, I, P, P, P, I, P, P, SZ, P], I),
         "moe_permute_workspace_bytes": ([I64, I, I, I, PSZ], I),
         "moe_permute": ([P, P, I64, I, I, I, I, I, P, P, P, P, P, P, SZ, P], I),
+        "moe_permute_noalloc": ([P, P, I64, I, I, I, I, I, P, P, P, P, P, P], I),
         "moe_grouped_swiglu_workspace_bytes": ([I64, I, I, I, U, PSZ], I),
         "moe_grouped_swiglu_fwd": ([P, P, I, I64, I, I, P, P, P, P, P, P, P, SZ, P], I),
         "moe_grouped_swiglu_bwd": ([P, P, P, P, P, I, I64, I, I, P, P, P, P, P, P, P, U, P, SZ,
@@ -229,6 +231,34 @@ def moe_permute(x, topk_idx, E, expert_begin=0, num_local=None, cap=None, counts
                            _ptr(ws), ws.numel(), _stream()), "moe_permute")
     return {"expert_offsets": offsets, "counts_global": cg, "row_src": row_src,
             "dst": dst[: T * k].view(T, k), "x_perm": x_perm, "cap": cap}
+
+
+def moe_permute_noalloc(x, topk_idx, E, expert_begin=0, num_local=None, out=None,
+                        counts_global=True):
+    """moe_permute on the library's static scratch (no workspace).  `out`:
+    optional dict of preallocated outputs as moe_permute returns them
+    (expert_offsets, counts_global, row_src, dst, x_perm); otherwise they
+    are allocated here.  Returns that dict."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(topk_idx, torch.int32, "topk_idx", 2)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    num_local = E if num_local is None else num_local
+    dev = x.device
+    if out is None:
+        cap = T * min(k, num_local)
+        out = {"expert_offsets": torch.empty(num_local + 1, dtype=torch.int32, device=dev),
+               "counts_global": torch.empty(E, dtype=torch.int32, device=dev)
+               if counts_global else None,
+               "row_src": torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
+               "dst": torch.empty(max(T * k, 1), dtype=torch.int32, device=dev),
+               "x_perm": torch.empty((max(cap, 1), d), dtype=torch.bfloat16, device=dev),
+               "cap": cap}
+    _check(lib.moe_permute_noalloc(_ptr(x), _ptr(topk_idx), T, d, E, k, expert_begin, num_local,
+                                   _ptr(out["expert_offsets"]), _ptr(out.get("counts_global")),
+                                   _ptr(out["row_src"]), _ptr(out["dst"]), _ptr(out["x_perm"]),
+                                   _stream()), "moe_permute_noalloc")
+    return out
 
 
 # ----------------------------------------------------- grouped SwiGLU FFN

@@ -136,6 +136,9 @@ Z = None
                                                         P, P, P, P, Z)),
     ("llep dispatch E_p", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 5, 0, 10, 64, 12, 2, 5,
                                                         P, P, P, P, Z)),
+    ("noalloc range", lambda L: L.moe_permute_noalloc(P, P, 10, 64, 8, 2, 4, 8, P, Z, P, P, P, Z)),
+    ("noalloc null offsets", lambda L: L.moe_permute_noalloc(P, P, 10, 64, 8, 2, 0, 8, Z, Z, P, P,
+                                                            P, Z)),
 ])
 def test_invalid_arguments_rejected_on_host(lib, case):
     name, call = case
@@ -153,6 +156,20 @@ def test_workspace_too_small_rejected(lib):
                                    Z) == -3
     assert lib.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
     assert lib.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="dummy pointers are only safe without a GPU")
+def test_noalloc_permute_rejects_sizes_beyond_its_scratch(lib):
+    """moe_permute_noalloc refuses, on the host, sizes whose scratch would
+    exceed MOE_PERMUTE_NOALLOC_MAX_BYTES (8 MiB): 2^24 assignments over 1024
+    experts need 4096 blocks x 3 x 1024 counts = 48 MiB."""
+    n = ctypes.c_size_t()
+    assert lib.moe_permute_workspace_bytes(1 << 24, 1024, 1, 1024, ctypes.byref(n)) == 0
+    assert n.value > 8 << 20
+    assert lib.moe_permute_noalloc(P, P, 1 << 24, 64, 1024, 1, 0, 1024, P, Z, P, P, P, Z) == -2
+    assert b"MOE_PERMUTE_NOALLOC_MAX_BYTES" in lib.moe_last_error()
+    assert lib.moe_permute_workspace_bytes(65536, 128, 8, 128, ctypes.byref(n)) == 0
+    assert n.value <= 8 << 20  # the long-context workload fits
 
 
 def test_vocab_workspace_is_one_block_of_gradients():
