@@ -324,6 +324,136 @@ struct NOperand {
   }
 };
 
+// ------------------------------------------------- per-tile load streams
+// The loads of one operand of one tile, prepared once when the tile starts,
+// so that a K step's loads cost a source pick, an offset add and the loads
+// themselves.  Any step can be issued in any order (nothing advances per
+// issue).
+
+// K-contiguous operand.  Load q (0 .. LOADS_K - 1) of wave w, I = LOADS_K w
+// + q, fills tile rows 8 I .. 8 I + 7: lane l takes row 8 I + l / 8 and the
+// 16-byte chunk lc = (l % 8) ^ ((row / 2) % 8), which is lc0 for even q and
+// lc0 ^ 4 for odd q.  A lane whose row lies past the tile's valid rows gets
+// an offset past every descriptor range (it reads zeros); only a step that
+// reaches past the valid k masks chunks.  DUALK: steps [0, nk0) read source
+// 0, the rest source 1 (k restarting at 0).
+template <bool DUALK>
+struct KStream {
+  i32x4 rs0, rs1;
+  uint32_t voff[LOADS_K];  // lane offset of load q at k = 0
+  int nk0, km0, km1;
+  __device__ __forceinline__ void setup(const KOperand& op, int wave, int lane) {
+    rs0 = op.rsrc0;
+    rs1 = op.rsrc1;
+    nk0 = op.nk0;
+    km0 = op.kmax0;
+    km1 = op.kmax1;
+    const int rl = lane >> 3;
+    const int lc0 = (lane & 7) ^ (lane >> 4);
+#pragma unroll
+    for (int q = 0; q < LOADS_K; ++q) {
+      const int row = (wave * LOADS_K + q) * 8 + rl;
+      const int lc = (q & 1) ? (lc0 ^ 4) : lc0;
+      voff[q] = row < op.rows ? static_cast<uint32_t>(row) * op.ld + static_cast<uint32_t>(lc * 16)
+                              : OOB;
+    }
+  }
+  // step j of the tile into the LDS unit at `u`
+  __device__ __forceinline__ void issue(int j, uint32_t u, int wave) const {
+    const bool s1 = DUALK && j >= nk0;
+    const int k0 = (s1 ? j - nk0 : j) * BK;
+    const int km = s1 ? km1 : km0;
+    const i32x4 rs = s1 ? rs1 : rs0;
+    const uint32_t kb = static_cast<uint32_t>(k0) * 2u;
+    if (k0 + BK <= km) {
+#pragma unroll
+      for (int q = 0; q < LOADS_K; ++q) load_lds16(rs, voff[q] + kb, u + (wave * LOADS_K + q) * 1024);
+    } else {
+      const int lane = opaque(static_cast<int>(threadIdx.x & 63));
+      const int lc0 = (lane & 7) ^ (lane >> 4);
+#pragma unroll
+      for (int q = 0; q < LOADS_K; ++q) {
+        const int lc = (q & 1) ? (lc0 ^ 4) : lc0;
+        load_lds16(rs, k0 + lc * 8 < km ? voff[q] + kb : OOB, u + (wave * LOADS_K + q) * 1024);
+      }
+    }
+  }
+  // the same number of loads, all out of range (zeros into an unused slot)
+  static __device__ __forceinline__ void none(const i32x4& nil, uint32_t u, int wave) {
+#pragma unroll
+    for (int q = 0; q < LOADS_K; ++q) load_lds16(nil, OOB, u + (wave * LOADS_K + q) * 1024);
+  }
+};
+
+// N-contiguous operand: this wave's sub-tile of 128 columns (waves 0-3 load
+// sub-tile 0, waves 4-7 sub-tile 1).  Half h (0, 1) of step j covers rows r0
+// = 64 j + 32 h .. r0 + 31; load Q (0 .. LOADS_H - 1), I = LOADS_H w + Q,
+// covers rows r0 + kr .. +3, kr = 4 (I % 8): lane l takes row r0 + kr + l / 16
+// and column 8 ((l % 16) ^ (4 (l / 16))).  The descriptor's base moves to row
+// r0 (64-bit, so lane offsets stay below 32 rows at any K) while its range
+// stays the bound set at the tile's start: every lane's column and row are
+// checked, so valid lanes never reach it.  Lanes of columns past the
+// sub-tile's valid columns get an out-of-range offset; only a half that
+// reaches past the valid k masks rows.
+struct NStream {
+  uint64_t base;           // byte address of the sub-tile's row 0
+  uint32_t range, ld;      // descriptor range from row 0; row pitch in bytes
+  uint32_t voff[LOADS_H];  // lane offset of load Q from the half's first row
+  int kmax;
+  __device__ __forceinline__ void setup(const NOperand& op, int wave, int lane) {
+    const int sub = (wave * LOADS_H) >> 3;
+    const i32x4 r = make_rsrc(sub ? op.ptr1 : op.ptr0, sub ? op.range1 : op.range0);
+    base = (static_cast<uint64_t>(static_cast<uint32_t>(r[1]) & 0xffffu) << 32) |
+           static_cast<uint32_t>(r[0]);
+    range = static_cast<uint32_t>(r[2]);
+    ld = op.ld;
+    kmax = op.kmax;
+    const int kl = lane >> 4;
+    const int col = ((lane & 15) ^ (4 * kl)) * 8;
+    const int cols = sub ? op.cols1 : op.cols0;
+#pragma unroll
+    for (int q = 0; q < LOADS_H; ++q) {
+      const int kr = ((wave * LOADS_H + q) & 7) * 4;
+      voff[q] = col < cols ? static_cast<uint32_t>(kr + kl) * ld + static_cast<uint32_t>(col * 2)
+                           : OOB;
+    }
+  }
+  // half h of step j into the LDS half at `u` (both sub-tiles' halves)
+  __device__ __forceinline__ void issue(int j, int h, uint32_t u, int wave) const {
+    const int sub = (wave * LOADS_H) >> 3;
+    const int r0 = j * BK + h * (BK / 2);
+    const uint64_t a = base + static_cast<uint64_t>(static_cast<uint32_t>(r0)) * ld;
+    i32x4 rs;
+    rs[0] = static_cast<int>(a & 0xffffffffu);
+    rs[1] = static_cast<int>((a >> 32) & 0xffffu);
+    rs[2] = static_cast<int>(range);
+    rs[3] = 0x00020000;
+    const int krem = kmax - r0;
+    if (krem >= BK / 2) {
+#pragma unroll
+      for (int q = 0; q < LOADS_H; ++q) {
+        const int I = wave * LOADS_H + q;
+        load_lds16(rs, voff[q], u + sub * (HALF / 2) + (I & 7) * 1024);
+      }
+    } else {
+      const int kl = opaque(static_cast<int>(threadIdx.x & 63)) >> 4;
+#pragma unroll
+      for (int q = 0; q < LOADS_H; ++q) {
+        const int I = wave * LOADS_H + q;
+        const int kr = (I & 7) * 4;
+        load_lds16(rs, kl < krem - kr ? voff[q] : OOB, u + sub * (HALF / 2) + (I & 7) * 1024);
+      }
+    }
+  }
+  static __device__ __forceinline__ void none(const i32x4& nil, uint32_t u, int wave) {
+#pragma unroll
+    for (int q = 0; q < LOADS_H; ++q) {
+      const int I = wave * LOADS_H + q;
+      load_lds16(nil, OOB, u + (I >> 3) * (HALF / 2) + (I & 7) * 1024);
+    }
+  }
+};
+
 struct GemmArgs {
   // inputs
   const uint16_t* x_perm;   // [cap][d]
@@ -1092,10 +1222,11 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   struct Frags {
     bf16x8 a[4], b[2];
   };
-  // fragments of sub-step `sub` (16 k, 0..3) of stream step `s`
-  auto load_frags = [&](Frags& F, int s, int sub) __attribute__((always_inline)) {
-    const lds_char* ta = ring + (s % NA) * UNIT + (A_N ? (sub >> 1) * HALF : 0);
-    const lds_char* tb = ring + (NA + s % NB) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
+  // fragments of sub-step `sub` (16 k, 0..3) of the step held in A's ring
+  // slot `sa` and B's ring slot `sb`
+  auto load_frags = [&](Frags& F, int sa, int sb, int sub) __attribute__((always_inline)) {
+    const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
+    const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if constexpr (A_N) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
@@ -1116,152 +1247,88 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   };
 
   // ---------------------------------------------------------- tile stream
-  // The workgroup's tiles form one stream of K steps, walked by three tile
-  // iterators: one for the MFMAs and one per operand for the loads, which
-  // run ahead across tile boundaries.  Past the end of the stream the load
-  // iterators issue the same number of loads out of range (they write zeros
-  // to slots nobody reads), which keeps every sync's count exact.  After a
-  // tile's last step, B's slot of that step holds the epilogue patches; the
-  // refill of that slot waits until the epilogue is done.
+  // Tiles run one after another, each with its own K loop; A is loaded one
+  // step and B two steps ahead of the sync that needs them.  Near a tile's
+  // end those loads fetch the next tile's first steps (its load streams are
+  // prepared when the current tile starts).  A load that would reach still
+  // further (the next tile has fewer steps than the look-ahead) is issued
+  // out of range into its slot, so every sync's count stays exact, and is
+  // issued again for real when its tile starts, after a full wait.  After a
+  // tile's last step, B's slot of that step holds the epilogue patches; its
+  // refill waits for the epilogue.
+  using AStream = typename std::conditional<A_N, NStream, KStream<MODE == DGRAD_GATE_UP>>::type;
+  using BStream = typename std::conditional<B_N, NStream, KStream<MODE == DGRAD_GATE_UP>>::type;
   const Tables tb{g.mt_start, g.offsets, g.wk_start, g.nz_start};
   const i32x4 nil = make_rsrc(nullptr, 0);
-  TileIter<MODE> itc, ita, itb;
-  itc.init(g, tb);
-  ita.init(g, tb);
-  itb.init(g, tb);
+  TileIter<MODE> it;
+  it.init(g, tb);
   zero_acc();
-  Tile tc = itc.next(g, tb);
+  Tile tc = it.next(g, tb);
   if (tc.valid) {
-    Tile tla = ita.next(g, tb), tlb = itb.next(g, tb);
-    AOp A;
-    BOp B;
-    bool hava = false, havb = false;
-    int kta = 0, ktb = 0, ga = 0, gb = 0;  // step within the load tile; stream step
-    // Each operand's load stream advances one issue at a time: a K-contiguous
-    // unit (h = -1) or the low / high half (h = 0 / 1) of an N-contiguous
-    // step.  `next_issue` moves the stream to that issue's tile and returns
-    // the LDS address it fills (-1: past the end of the stream).
-    auto next_issueA = [&](int h) __attribute__((always_inline)) {
-      if (h <= 0 && tla.valid && kta >= tla.nk) {
-        tla = ita.next(g, tb);
-        kta = 0;
-        hava = false;
-      }
-      if (tla.valid && !hava) {
-        setupA(tla, A);
-        if constexpr (A_N) A.start();
-        hava = true;
-      }
-      return lds0 + (ga % NA) * UNIT + (h > 0 ? HALF : 0);
+    AStream sa, xa;  // loads of this tile and of the next one
+    BStream sb, xb;
+    auto prep = [&](const Tile& t, AStream& a, BStream& b) __attribute__((always_inline)) {
+      AOp ao;
+      setupA(t, ao);
+      a.setup(ao, w, lane);
+      BOp bo;
+      setupB(t, bo);
+      b.setup(bo, w, lane);
     };
-    auto next_issueB = [&](int h) __attribute__((always_inline)) {
-      if (h <= 0 && tlb.valid && ktb >= tlb.nk) {
-        tlb = itb.next(g, tb);
-        ktb = 0;
-        havb = false;
-      }
-      if (tlb.valid && !havb) {
-        setupB(tlb, B);
-        if constexpr (B_N) B.start();
-        havb = true;
-      }
-      return lds0 + (NA + gb % NB) * UNIT + (h > 0 ? HALF : 0);
+    // part p (0, 1) of one step's loads of an operand into ring slot `slot`:
+    // the two halves of an N-contiguous step; a K-contiguous step at p = 0
+    auto issA = [&](const AStream& st, int j, int slot, int p) __attribute__((always_inline)) {
+      const uint32_t u = lds0 + slot * UNIT;
+      if constexpr (A_N) st.issue(j, p, u + p * HALF, w);
+      else if (p == 0) st.issue(j, u, w);
     };
-    auto done_issueA = [&](int h) __attribute__((always_inline)) {
-      if (h != 0) {
-        ++kta;
-        ++ga;
-      }
+    auto noneA = [&](int slot, int p) __attribute__((always_inline)) {
+      const uint32_t u = lds0 + slot * UNIT;
+      if constexpr (A_N) NStream::none(nil, u + p * HALF, w);
+      else if (p == 0) KStream<false>::none(nil, u, w);
     };
-    auto done_issueB = [&](int h) __attribute__((always_inline)) {
-      if (h != 0) {
-        ++ktb;
-        ++gb;
-      }
+    auto issB = [&](const BStream& st, int j, int slot, int p) __attribute__((always_inline)) {
+      const uint32_t u = lds0 + (NA + slot) * UNIT;
+      if constexpr (B_N) st.issue(j, p, u + p * HALF, w);
+      else if (p == 0) st.issue(j, u, w);
     };
-    // K-contiguous operands: prep returns the issue's loads, which the caller
-    // emits.
-    struct NoIssue {};
-    using AIssue = typename std::conditional<A_N, NoIssue, KOperand::Issue>::type;
-    using BIssue = typename std::conditional<B_N, NoIssue, KOperand::Issue>::type;
-    struct StepA {
-      AIssue p0;
+    auto noneB = [&](int slot, int p) __attribute__((always_inline)) {
+      const uint32_t u = lds0 + (NA + slot) * UNIT;
+      if constexpr (B_N) NStream::none(nil, u + p * HALF, w);
+      else if (p == 0) KStream<false>::none(nil, u, w);
     };
-    struct StepB {
-      BIssue p0;
-    };
-    auto prep_stepA = [&]() __attribute__((always_inline)) {
-      StepA st;
-      if constexpr (A_K) {
-        const uint32_t base = next_issueA(-1);
-        st.p0 = tla.valid ? A.prep(kta, base, lane) : KOperand::none(nil, base);
-        done_issueA(-1);
-      }
-      return st;
-    };
-    auto prep_stepB = [&]() __attribute__((always_inline)) {
-      StepB st;
-      if constexpr (B_K) {
-        const uint32_t base = next_issueB(-1);
-        st.p0 = tlb.valid ? B.prep(ktb, base, lane) : KOperand::none(nil, base);
-        done_issueB(-1);
-      }
-      return st;
-    };
-    // load q (0 .. 3) of a K-contiguous step's issue
-    auto emitA = [&](const StepA& st, int q) __attribute__((always_inline)) {
-      if constexpr (A_K) st.p0.emit(q, w);
-    };
-    auto emitB = [&](const StepB& st, int q) __attribute__((always_inline)) {
-      if constexpr (B_K) st.p0.emit(q, w);
-    };
-    // Part p (0, 1) of a step's loads of an operand: an N-contiguous half,
-    // straight from the operand's stream; a K-contiguous unit is part 0.
-    auto issue_partA = [&](int p) __attribute__((always_inline)) {
-      if constexpr (A_N) {
-        const uint32_t base = next_issueA(p);
-        if (tla.valid) A.issue(base, lane, w);
-        else NOperand::issue_none(nil, base, w);
-        done_issueA(p);
-      } else if (p == 0) {
-        const StepA st = prep_stepA();
-        static_for<LA>([&](auto Q) { emitA(st, Q); });
-      }
-    };
-    auto issue_partB = [&](int p) __attribute__((always_inline)) {
-      if constexpr (B_N) {
-        const uint32_t base = next_issueB(p);
-        if (tlb.valid) B.issue(base, lane, w);
-        else NOperand::issue_none(nil, base, w);
-        done_issueB(p);
-      } else if (p == 0) {
-        const StepB st = prep_stepB();
-        static_for<LB>([&](auto Q) { emitB(st, Q); });
-      }
-    };
-    auto issue_stepA = [&]() __attribute__((always_inline)) {
-      issue_partA(0);
-      issue_partA(1);
-    };
-    auto issue_stepB = [&]() __attribute__((always_inline)) {
-      issue_partB(0);
-      issue_partB(1);
-    };
-    // The 8 MFMAs that follow a sync with the step's loads between them (F's
-    // parts, then S's), so that the matrix cores have work while the loads
-    // are issued.
-    auto mma_issue = [&](const Frags& F) __attribute__((always_inline)) {
-      static_for<8>([&](auto T) {
-        constexpr int t = T;
-        acc[t / 2][t % 2] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (t % 2 == 1) {
-          if constexpr (t < 4) issue_partA(t / 2);
-          else issue_partB(t / 2 - 2);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      });
+
+    prep(tc, sa, sb);
+    // prologue: the loads the syncs of steps -3, -2, -1 would have issued
+    // (B 0; A 0, B 1; A 1, B 2), steps past the tile out of range
+    {
+      const int nk = tc.nk;
+      auto pa = [&](int j) {
+        static_for<2>([&](auto P) {
+          if (j < nk) issA(sa, j, j, P); else noneA(j, P);
+        });
+      };
+      auto pb = [&](int j) {
+        static_for<2>([&](auto P) {
+          if (j < nk) issB(sb, j, j, P); else noneB(j, P);
+        });
+      };
+      pb(0);
+      pa(0);
+      pb(1);
+      pa(1);
+      pb(2);
+    }
+    wait_vmcnt<X_END>();
+    lgkm_drained();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+
+    Frags cur, nxt;
+    int ra = 0, rb = 0;  // ring slots (A: 0..1, B: 0..2) of the step being computed
+    load_frags(cur, 0, 0, 0);
+    auto sync = [&]() __attribute__((always_inline)) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
     };
     // the 8 MFMAs of one sub-step, kept in this order
     auto mma_seq = [&](const Frags& F) __attribute__((always_inline)) {
@@ -1272,65 +1339,104 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         __builtin_amdgcn_sched_barrier(0);
       });
     };
-    // prologue: the issues the syncs of steps -3, -2, -1 would have made
-    // (F before S)
-    static_for<3>([&](auto V) {
-      constexpr int v = static_cast<int>(V) - 3;
-      if constexpr (v + NA >= 0) issue_stepA();
-      if constexpr (v + NB >= 0) issue_stepB();
-    });
-    wait_vmcnt<X_END>();
-    lgkm_drained();
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-
-    Frags cur, nxt;
-    int s = 0;  // stream step being computed
-    load_frags(cur, 0, 0);
-    auto sync = [&]() __attribute__((always_inline)) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
-    };
-    // one K step; `last`: last step of the tile (its sync defers the refill of
-    // the patch slot)
-    auto step = [&](auto LAST) __attribute__((always_inline)) {
-      constexpr bool last = LAST;
-      load_frags(nxt, s, 1);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_seq(cur);
-      __builtin_amdgcn_sched_barrier(0);
-      load_frags(cur, s, 2);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_seq(nxt);
-      __builtin_amdgcn_sched_barrier(0);
-      load_frags(nxt, s, 3);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_seq(cur);
-      __builtin_amdgcn_sched_barrier(0);
-      sync();
-      wait_vmcnt<X_END>();
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (!last) {
-        lgkm_drained();
-        load_frags(cur, s + 1, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_issue(nxt);
-        lgkm_drained();
-      } else {
-        // F goes out now; S's refill would land in the epilogue patches
-        issue_stepA();
-        __builtin_amdgcn_sched_barrier(0);
-        mma(nxt);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      ++s;
-    };
     while (true) {
-      for (int kk = 0; kk + 1 < tc.nk; ++kk) step(std::false_type{});
-      step(std::true_type{});
-      // epilogue patches: S's (B's) slot of the tile's last step
-      const int ls = s - 1;
-      lds_char* const patch = ring + (NA + ls % NB) * UNIT + w * PATCH_BYTES;
+      const int nk = tc.nk;
+      Tile tn;
+      tn.valid = false;
+      int nkn = 0;
+      unsigned done_a = 0, done_b = 0;  // steps of the next tile loaded for real
+      // part p of the A / B loads aimed at tile step j (past nk: the next tile)
+      auto loadA = [&](int j, int slot, int p) __attribute__((always_inline)) {
+        if (j < nk) {
+          issA(sa, j, slot, p);
+        } else if (j - nk < nkn) {
+          issA(xa, j - nk, slot, p);
+          done_a |= 1u << (j - nk);
+        } else {
+          noneA(slot, p);
+        }
+      };
+      auto loadB = [&](int j, int slot, int p) __attribute__((always_inline)) {
+        if (j < nk) {
+          issB(sb, j, slot, p);
+        } else if (j - nk < nkn) {
+          issB(xb, j - nk, slot, p);
+          done_b |= 1u << (j - nk);
+        } else {
+          noneB(slot, p);
+        }
+      };
+      // One K step.  TAIL: its look-ahead loads may reach past the tile
+      // (the next tile or nothing); otherwise they stay inside it.  LAST:
+      // the tile's last step (B's refill waits for the epilogue).
+      auto step = [&](int ks, auto TAIL, auto LAST) __attribute__((always_inline)) {
+        constexpr bool tail = TAIL, last = LAST;
+        const int ra1 = ra ^ 1, rb1 = rb == 2 ? 0 : rb + 1;  // slots of the next step
+        load_frags(nxt, ra, rb, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_seq(cur);
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(cur, ra, rb, 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_seq(nxt);
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(nxt, ra, rb, 3);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_seq(cur);
+        __builtin_amdgcn_sched_barrier(0);
+        sync();
+        wait_vmcnt<X_END>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // this step's slots are free: A's refill with step ks + 2, B's with
+        // ks + 3 (deferred past the epilogue on the tile's last step)
+        if constexpr (!last) {
+          lgkm_drained();
+          load_frags(cur, ra1, rb1, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          // the 8 MFMAs of sub-step 3 with the loads between them (A's parts
+          // after the second and fourth, B's after the sixth and eighth)
+          static_for<8>([&](auto T) {
+            constexpr int t = T;
+            acc[t / 2][t % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                nxt.b[t % 2], nxt.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (t % 2 == 1) {
+              if constexpr (t < 4) {
+                if constexpr (tail) loadA(ks + 2, ra, t / 2);
+                else issA(sa, ks + 2, ra, t / 2);
+              } else {
+                if constexpr (tail) loadB(ks + 3, rb, t / 2 - 2);
+                else issB(sb, ks + 3, rb, t / 2 - 2);
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          });
+          lgkm_drained();
+        } else {
+          loadA(ks + 2, ra, 0);
+          loadA(ks + 2, ra, 1);
+          __builtin_amdgcn_sched_barrier(0);
+          mma(nxt);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        ra = ra1;
+        rb = rb1;
+      };
+      int ks = 0;
+      // steps whose loads stay inside the tile
+      for (; ks + NB < nk; ++ks) step(ks, std::false_type{}, std::false_type{});
+      // the last steps reach into the next tile: prepare its loads now
+      tn = it.next(g, tb);
+      if (tn.valid) {
+        prep(tn, xa, xb);
+        nkn = tn.nk;
+      }
+      for (; ks + 1 < nk; ++ks) step(ks, std::true_type{}, std::false_type{});
+      step(ks, std::true_type{}, std::true_type{});
+      // epilogue patches: B's slot of the tile's last step
+      const int rlast = rb == 0 ? 2 : rb - 1;
+      lds_char* const patch = ring + (NA + rlast) * UNIT + w * PATCH_BYTES;
       epilogue(tc, patch);
       zero_acc();
       // the patch reads are done once the LDS counter drains; the stores stay
@@ -1338,12 +1444,41 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       __builtin_amdgcn_s_barrier();  // every wave is done with its patch
       __builtin_amdgcn_sched_barrier(0);
-      tc = itc.next(g, tb);
-      if (!tc.valid) break;
-      issue_stepB();  // S's deferred refill
+      if (!tn.valid) break;
+      // B's deferred refill (tile step nk + 2 = the next tile's step 2)
+      loadB(nk + 2, rlast, 0);
+      loadB(nk + 2, rlast, 1);
+      tc = tn;
+      sa = xa;
+      sb = xb;
+      // Steps of the new tile that a shorter tile before it could not load
+      // ahead went out as out-of-range loads: issue them now into their
+      // slots and wait for every load (rare: only after tiles of fewer
+      // steps than the look-ahead).
+      const unsigned need_a = (1u << min(tc.nk, NA)) - 1u, need_b = (1u << min(tc.nk, NB)) - 1u;
+      if ((done_a & need_a) != need_a || (done_b & need_b) != need_b) {
+        for (int j = 0; j < min(tc.nk, NA); ++j)
+          if (!((done_a >> j) & 1u)) {
+            const int sl = (ra + j) & 1;
+            issA(sa, j, sl, 0);
+            issA(sa, j, sl, 1);
+          }
+        for (int j = 0; j < min(tc.nk, NB); ++j)
+          if (!((done_b >> j) & 1u)) {
+            const int sl = (rb + j) % 3;
+            issB(sb, j, sl, 0);
+            issB(sb, j, sl, 1);
+          }
+        wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+      }
       lgkm_drained();
-      load_frags(cur, s, 0);
+      load_frags(cur, ra, rb, 0);
     }
+    // the last steps' out-of-range loads still write their (zero) slots:
+    // let them land before the workgroup's LDS is released
+    wait_vmcnt<0>();
   }
   if constexpr (WGRAD) {
     // experts without rows: their weight gradients are exact zeros
