@@ -14,11 +14,15 @@
 //     branching.
 //   * K steps of 64 through a ring of five 32 KiB LDS slots (all 160 KiB):
 //     two for operand A (loaded one step ahead) and three for operand B (two
-//     steps ahead); a sync's loads go out between the eight MFMAs that follow
-//     it; one barrier per step, and the stream of K steps continues across
-//     tile boundaries.  A step of 64 k makes every row of a K-contiguous
-//     tile one full 128-byte line, which the memory path moves at twice the
-//     rate of 64-byte halves.
+//     steps ahead); one barrier per step.  Each operand's loads of a tile
+//     are prepared once when the tile starts (descriptors in scalar
+//     registers, lane offsets in vector registers), so a step's loads cost
+//     little more than the loads themselves; they go out between the MFMAs
+//     that follow the barrier, and the next sub-step's fragment reads go out
+//     one by one between the current sub-step's MFMAs.  Near a tile's end the
+//     look-ahead loads fetch the next tile's first steps.  A step of 64 k
+//     makes every row of a K-contiguous tile one full 128-byte line, which
+//     the memory path moves at twice the rate of 64-byte halves.
 //   * Operands stored K-contiguous (activations in the forward pass and the
 //     data gradients, weights in the data gradients) sit in LDS as
 //     [256 rows][64 k] and feed the MFMA with ds_read_b128.  Operands stored
@@ -34,9 +38,11 @@
 //     gets no forward tiles and zero weight gradients.
 //   * XCD-aware order: gfx950 hands consecutive workgroups to its 8 XCDs in
 //     turn, and each XCD has its own L2.  Logical tiles are laid out so each
-//     XCD runs a contiguous range of them, and inside one expert the row
-//     tiles of one weight tile are adjacent: they share that weight tile in
-//     the same L2, so each weight byte comes from HBM about once.
+//     XCD runs a contiguous range of them, walked in groups of 8 row tiles:
+//     the 32 tiles an XCD runs at a time form an 8 x 4 block of one expert
+//     that shares 8 row slabs and 4 column slabs of the operands in that L2.
+//   * Dense modes run the same loop on plain products (the router's
+//     backward and the blockwise vocabulary loss) with their own epilogues.
 #include "common.h"
 
 namespace moe {
@@ -112,10 +118,18 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* p, int64_t bytes) {
 // 16 bytes per lane, global -> LDS; lane i writes LDS [lds + 16 i, +16).
 // Issued as inline asm so the compiler does not wait for it at every
 // barrier; completion is tracked by hand with vmcnt.
+// The descriptor and LDS address are wave-uniform; readfirstlane states it
+// so that they always reach the instruction in scalar registers.
 __device__ __forceinline__ void load_lds16(const i32x4& rsrc, uint32_t voff, uint32_t lds) {
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane(rsrc[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(rsrc[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(rsrc[2]);
+  r[3] = __builtin_amdgcn_readfirstlane(rsrc[3]);
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
-               : "s"(lds), "v"(voff), "s"(rsrc)
+               : "s"(l), "v"(voff), "s"(r)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -178,54 +192,6 @@ struct KOperand {
   int kmax0, kmax1; // valid k of source 0 / 1
   int nk0;          // steps of source 0
 
-  // Load q (0 .. LOADS_K - 1) of this wave, I = LOADS_K wave + q, fills tile
-  // rows 8 I .. 8 I + 7: lane l takes row r = 8 I + l / 8 and 16-byte chunk
-  // lc = (l % 8) ^ ((r / 2) % 8), where (r / 2) % 8 = 4 (q % 2) + l / 16.
-  // prep() computes what the loads of one step share; Issue::emit(q) sends
-  // load q.
-  struct Issue {
-    i32x4 rs;
-    uint32_t ld, lds;     // row pitch; LDS base of the unit
-    uint32_t vb0, vb1;    // lane offsets of even / odd loads
-    int rows, rl;         // valid tile rows; this lane's row within a load
-    bool kok0, kok1;      // this lane's chunk lies below K (even / odd loads)
-    __device__ __forceinline__ void emit(int q, int wave) const {
-      const int r0 = (wave * LOADS_K + q) * 8;
-      const bool ok = ((q & 1) ? kok1 : kok0) && rl < rows - r0;
-      load_lds16(rs, ok ? ((q & 1) ? vb1 : vb0) + static_cast<uint32_t>(r0) * ld : OOB,
-                 lds + (wave * LOADS_K + q) * 1024);
-    }
-  };
-  __device__ __forceinline__ Issue prep(int kt, uint32_t lds_op, int lane_in) const {
-    const bool s1 = kt >= nk0;
-    const int k0 = (s1 ? kt - nk0 : kt) * BK;
-    const int km = s1 ? kmax1 : kmax0;
-    Issue p;
-    p.rs = s1 ? rsrc1 : rsrc0;
-    const int lane = opaque(lane_in);
-    p.rl = lane >> 3;
-    const int lc0 = (lane & 7) ^ (lane >> 4);      // chunk fetched by even loads
-    const int lc1 = lc0 ^ 4;                       //                 odd loads
-    p.kok0 = k0 + lc0 * 8 < km;
-    p.kok1 = k0 + lc1 * 8 < km;
-    const uint32_t rb = static_cast<uint32_t>(p.rl) * ld + static_cast<uint32_t>(k0 * 2);
-    p.vb0 = rb + static_cast<uint32_t>(lc0 * 16);
-    p.vb1 = rb + static_cast<uint32_t>(lc1 * 16);
-    p.ld = ld;
-    p.rows = rows;
-    p.lds = lds_op;
-    return p;
-  }
-  // the same number of loads, all out of range (zeros into an unused slot)
-  static __device__ __forceinline__ Issue none(const i32x4& nil, uint32_t lds_op) {
-    Issue p;
-    p.rs = nil;
-    p.ld = p.vb0 = p.vb1 = 0;
-    p.rows = p.rl = 0;
-    p.kok0 = p.kok1 = false;
-    p.lds = lds_op;
-    return p;
-  }
   // MFMA fragment: 8 consecutive k (k-group `kg` of substep s) of tile row r
   static __device__ __forceinline__ bf16x8 frag(const lds_char* t, int r, int s, int kg) {
     return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(t + koff(r, 2 * s + kg));
@@ -237,25 +203,12 @@ struct KOperand {
 // k*ld + 2c of the sub-tile's base.  The tile's 256 columns are two
 // sub-tiles of 128 (sub-tile j starts at ptr_j, has cols_j valid columns and
 // range_j readable bytes); k < kmax valid.  Loads move half a step (32 k)
-// at a time, so that the half consumed first is refilled half a step
-// earlier.  The descriptor base advances with k (two scalar adds per
-// sub-tile and half), so lane offsets stay below 32 rows; every lane's row
-// and column are checked against krem and cols_j, so the descriptor range,
-// fixed at the tile's start, is only a bound that valid lanes never reach.  LDS per half: two sub-tiles [32 k][128 cols] bf16, 256-byte
+// at a time (the load stream below).  LDS per half: two sub-tiles [32 k][128
+// cols] bf16, 256-byte
 // rows, 16-byte chunk c of row k at ((c ^ (4 (k & 3))) << 4): the 32 lanes of
 // one ds_read_b64_tr_b16 pass (4 rows x 4 chunks x 2 halves) hit all 64 banks.
 __device__ __forceinline__ int noff(int k, int col) {
   return k * 256 + ((((col >> 3) ^ (4 * (k & 3)))) << 4) + ((col >> 2) & 1) * 8;
-}
-
-// base address (words 0-1 of a descriptor without stride) + bytes
-__device__ __forceinline__ i32x4 rsrc_advance(i32x4 r, uint32_t bytes) {
-  const uint64_t a =
-      ((static_cast<uint64_t>(static_cast<uint32_t>(r[1]) & 0xffffu) << 32) | static_cast<uint32_t>(r[0])) +
-      bytes;
-  r[0] = static_cast<int>(a & 0xffffffffu);
-  r[1] = static_cast<int>((a >> 32) & 0xffffu);
-  return r;
 }
 
 struct NOperand {
@@ -265,46 +218,6 @@ struct NOperand {
   uint32_t ld;
   int cols0, cols1;
   int kmax;
-  // load stream: descriptors of the next half's first row, valid k from there
-  i32x4 rn0, rn1;
-  int krem;
-  __device__ __forceinline__ void start() {
-    rn0 = make_rsrc(ptr0, range0);
-    rn1 = make_rsrc(ptr1, range1);
-    krem = kmax;
-  }
-
-  // This wave's loads of the next half (halves are issued in order from
-  // start()).  Load q (0 .. LOADS_H - 1), I = LOADS_H wave + q, covers rows
-  // 4 (I % 8) .. +3 of sub-tile I / 8 (the same for all of a wave's loads);
-  // lane l takes row k = 4 (I % 8) + l / 16 and column 8 ((l % 16) ^ (4 (k % 4))).
-  __device__ __forceinline__ void issue(uint32_t lds_half, int lane_in, int wave) {
-    static_assert(8 % LOADS_H == 0, "a wave's loads stay in one sub-tile");
-    const int lane = opaque(lane_in);
-    const int kl = lane >> 4;                        // row within the load's 4 rows
-    const int col = ((lane & 15) ^ (4 * kl)) * 8;    // (row % 4 == kl)
-    const uint32_t vb = static_cast<uint32_t>(kl) * ld + static_cast<uint32_t>(col) * 2u;
-    const int sub = (wave * LOADS_H) >> 3;
-    const i32x4 rs = sub ? rn1 : rn0;
-    const int cols = sub ? cols1 : cols0;
-    static_for<LOADS_H>([&](auto Q) {
-      const int I = wave * LOADS_H + Q;
-      const int kr = (I & 7) * 4;
-      const bool ok = col < cols && kl < krem - kr;
-      load_lds16(rs, ok ? vb + static_cast<uint32_t>(kr) * ld : OOB,
-                 lds_half + sub * (HALF / 2) + (I & 7) * 1024);
-    });
-    rn0 = rsrc_advance(rn0, (BK / 2) * ld);
-    rn1 = rsrc_advance(rn1, (BK / 2) * ld);
-    krem -= BK / 2;
-  }
-  // the same number of loads, all out of range (zeros into an unused slot)
-  static __device__ __forceinline__ void issue_none(const i32x4& nil, uint32_t lds_half, int wave) {
-    static_for<LOADS_H>([&](auto Q) {
-      const int I = wave * LOADS_H + Q;
-      load_lds16(nil, OOB, lds_half + (I >> 3) * (HALF / 2) + (I & 7) * 1024);
-    });
-  }
   // MFMA fragment of tile column block c0 (multiple of 32) from one half:
   // lane l gets 8 consecutive k (k-group l/32 of substep s, 0..1, of the
   // half) of column c0 + l%32, built from two transposing reads of 4 k each.
@@ -1238,6 +1151,19 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       else F.b[jj] = BOp::frag(tb, brow[jj], sub & 1, lane);
     }
   };
+  // one fragment f of sub-step `sub` (f = 0..3: A's row blocks, 4..5: B's)
+  auto load_frag1 = [&](Frags& F, int sa, int sb, int sub, auto FI) __attribute__((always_inline)) {
+    constexpr int f = FI;
+    if constexpr (f < 4) {
+      const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
+      if constexpr (A_N) F.a[f] = AOp::frag(ta, arow[f], sub & 1, lane);
+      else F.a[f] = AOp::frag(ta, arow[f] + l32, sub, lh);
+    } else {
+      const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
+      if constexpr (B_K) F.b[f - 4] = BOp::frag(tb, brow[f - 4] + l32, sub, lh);
+      else F.b[f - 4] = BOp::frag(tb, brow[f - 4], sub & 1, lane);
+    }
+  };
   auto mma = [&](const Frags& F) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -1330,6 +1256,21 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     auto sync = [&]() __attribute__((always_inline)) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
     };
+    // the 8 MFMAs of one sub-step on F, with the six fragment reads of the
+    // next sub-step (into G) spread between them so that the LDS sees a
+    // steady stream of requests
+    auto mma_read = [&](const Frags& F, Frags& G, int sa, int sb, int sub) __attribute__((always_inline)) {
+      static_for<8>([&](auto T) {
+        constexpr int t = T;
+        acc[t / 2][t % 2] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (t < 6) {
+          load_frag1(G, sa, sb, sub, std::integral_constant<int, t>{});
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+    };
     // the 8 MFMAs of one sub-step, kept in this order
     auto mma_seq = [&](const Frags& F) __attribute__((always_inline)) {
       static_for<8>([&](auto T) {
@@ -1372,18 +1313,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       auto step = [&](int ks, auto TAIL, auto LAST) __attribute__((always_inline)) {
         constexpr bool tail = TAIL, last = LAST;
         const int ra1 = ra ^ 1, rb1 = rb == 2 ? 0 : rb + 1;  // slots of the next step
-        load_frags(nxt, ra, rb, 1);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_seq(cur);
-        __builtin_amdgcn_sched_barrier(0);
-        load_frags(cur, ra, rb, 2);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_seq(nxt);
-        __builtin_amdgcn_sched_barrier(0);
-        load_frags(nxt, ra, rb, 3);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_seq(cur);
-        __builtin_amdgcn_sched_barrier(0);
+        mma_read(cur, nxt, ra, rb, 1);
+        mma_read(nxt, cur, ra, rb, 2);
+        mma_read(cur, nxt, ra, rb, 3);
         sync();
         wait_vmcnt<X_END>();
         __builtin_amdgcn_s_barrier();
