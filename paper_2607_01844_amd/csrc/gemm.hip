@@ -1257,16 +1257,20 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
     };
     // the 8 MFMAs of one sub-step on F, with the six fragment reads of the
-    // next sub-step (into G) spread between them so that the LDS sees a
-    // steady stream of requests
+    // next sub-step (into G) between the first three, in the order the next
+    // sub-step's MFMAs need them (a0 b0 | b1 a1 | a2 a3), so that each has
+    // five or more MFMAs to arrive
     auto mma_read = [&](const Frags& F, Frags& G, int sa, int sb, int sub) __attribute__((always_inline)) {
       static_for<8>([&](auto T) {
         constexpr int t = T;
         acc[t / 2][t % 2] =
             __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (t < 6) {
-          load_frag1(G, sa, sb, sub, std::integral_constant<int, t>{});
+        if constexpr (t < 3) {
+          constexpr int f0 = t == 0 ? 0 : t == 1 ? 5 : 2;
+          constexpr int f1 = t == 0 ? 4 : t == 1 ? 1 : 3;
+          load_frag1(G, sa, sb, sub, std::integral_constant<int, f0>{});
+          load_frag1(G, sa, sb, sub, std::integral_constant<int, f1>{});
           __builtin_amdgcn_sched_barrier(0);
         }
       });
