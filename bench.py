@@ -197,7 +197,8 @@ def chunked_forward(layer, steps: int):
     cap, d, f = wl.cap, wl.d, wl.f
     full_bytes = cap * (2 * d + 3 * f) * 2  # x_perm, y_perm, h_gate, h_up, act
     out = {"unchunked": {"ms": round(timed(unchunked), 4), "transient_bytes": full_bytes}}
-    for parts in (2, 4, 8):
+    # two buffer sets are live at once, so fewer than 4 chunks saves nothing
+    for parts in (4, 8, 16):
         chunk = -(-wl.T // parts)
         n = ctypes.c_size_t()
         m._check(m.lib.moe_ffn_fwd_chunked_workspace_bytes(chunk, wl.E, wl.k, wl.E_loc, d, f,
