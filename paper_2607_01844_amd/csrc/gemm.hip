@@ -23,6 +23,12 @@
 //     look-ahead loads fetch the next tile's first steps.  A step of 64 k
 //     makes every row of a K-contiguous tile one full 128-byte line, which
 //     the memory path moves at twice the rate of 64-byte halves.
+//   * The weight gradients (grouped, and the vocabulary's dW), which read
+//     both operands with transposing LDS reads, run the same ring in a
+//     ping-pong schedule when their tiles are long: the two waves of each
+//     SIMD take turns, one running a half step of MFMAs while the other
+//     issues loads and reads its next fragments, with a barrier between
+//     turns.
 //   * Operands stored K-contiguous (activations in the forward pass and the
 //     data gradients, weights in the data gradients) sit in LDS as
 //     [256 rows][64 k] and feed the MFMA with ds_read_b128.  Operands stored
@@ -55,8 +61,6 @@ constexpr int UNIT = 256 * BK * 2;  // one operand tile of one step in LDS (32 K
 constexpr int HALF = UNIT / 2;      // half a step (32 k) of an N-contiguous tile
 constexpr int NWAVE = 8;     // waves per workgroup: two per SIMD
 constexpr int NTHR = 64 * NWAVE;
-constexpr int LOADS_K = UNIT / 1024 / NWAVE;  // 16-byte direct loads per lane: K-contiguous unit
-constexpr int LOADS_H = HALF / 1024 / NWAVE;  //                                N-contiguous half
 constexpr int NRING = 5;     // LDS ring slots of UNIT bytes (160 KiB)
 constexpr int PATCH_BYTES = UNIT / NWAVE;  // per-wave epilogue staging (4 KiB)
 constexpr int NXCD = 8;
@@ -241,19 +245,21 @@ struct NOperand {
 // The loads of one operand of one tile, prepared once when the tile starts,
 // so that a K step's loads cost a source pick, an offset add and the loads
 // themselves.  Any step can be issued in any order (nothing advances per
-// issue).
+// issue).  NL waves (8: all of them, or 4: one group of the ping-pong
+// schedule) load one operand; `wave` is a wave's rank among them.
 
-// K-contiguous operand.  Load q (0 .. LOADS_K - 1) of wave w, I = LOADS_K w
-// + q, fills tile rows 8 I .. 8 I + 7: lane l takes row 8 I + l / 8 and the
-// 16-byte chunk lc = (l % 8) ^ ((row / 2) % 8), which is lc0 for even q and
-// lc0 ^ 4 for odd q.  A lane whose row lies past the tile's valid rows gets
-// an offset past every descriptor range (it reads zeros); only a step that
+// K-contiguous operand.  Load q (0 .. LK - 1) of wave w, I = LK w + q, fills
+// tile rows 8 I .. 8 I + 7: lane l takes row 8 I + l / 8 and the 16-byte
+// chunk lc = (l % 8) ^ ((row / 2) % 8), which is lc0 for even q and lc0 ^ 4
+// for odd q.  A lane whose row lies past the tile's valid rows gets an
+// offset past every descriptor range (it reads zeros); only a step that
 // reaches past the valid k masks chunks.  DUALK: steps [0, nk0) read source
 // 0, the rest source 1 (k restarting at 0).
-template <bool DUALK>
+template <bool DUALK, int NL>
 struct KStream {
+  static constexpr int LK = UNIT / 1024 / NL;  // 16-byte direct loads per lane and step
   i32x4 rs0, rs1;
-  uint32_t voff[LOADS_K];  // lane offset of load q at k = 0
+  uint32_t voff[LK];  // lane offset of load q at k = 0
   int nk0, km0, km1;
   __device__ __forceinline__ void setup(const KOperand& op, int wave, int lane) {
     rs0 = op.rsrc0;
@@ -264,8 +270,8 @@ struct KStream {
     const int rl = lane >> 3;
     const int lc0 = (lane & 7) ^ (lane >> 4);
 #pragma unroll
-    for (int q = 0; q < LOADS_K; ++q) {
-      const int row = (wave * LOADS_K + q) * 8 + rl;
+    for (int q = 0; q < LK; ++q) {
+      const int row = (wave * LK + q) * 8 + rl;
       const int lc = (q & 1) ? (lc0 ^ 4) : lc0;
       voff[q] = row < op.rows ? static_cast<uint32_t>(row) * op.ld + static_cast<uint32_t>(lc * 16)
                               : OOB;
@@ -280,41 +286,43 @@ struct KStream {
     const uint32_t kb = static_cast<uint32_t>(k0) * 2u;
     if (k0 + BK <= km) {
 #pragma unroll
-      for (int q = 0; q < LOADS_K; ++q) load_lds16(rs, voff[q] + kb, u + (wave * LOADS_K + q) * 1024);
+      for (int q = 0; q < LK; ++q) load_lds16(rs, voff[q] + kb, u + (wave * LK + q) * 1024);
     } else {
       const int lane = opaque(static_cast<int>(threadIdx.x & 63));
       const int lc0 = (lane & 7) ^ (lane >> 4);
 #pragma unroll
-      for (int q = 0; q < LOADS_K; ++q) {
+      for (int q = 0; q < LK; ++q) {
         const int lc = (q & 1) ? (lc0 ^ 4) : lc0;
-        load_lds16(rs, k0 + lc * 8 < km ? voff[q] + kb : OOB, u + (wave * LOADS_K + q) * 1024);
+        load_lds16(rs, k0 + lc * 8 < km ? voff[q] + kb : OOB, u + (wave * LK + q) * 1024);
       }
     }
   }
   // the same number of loads, all out of range (zeros into an unused slot)
   static __device__ __forceinline__ void none(const i32x4& nil, uint32_t u, int wave) {
 #pragma unroll
-    for (int q = 0; q < LOADS_K; ++q) load_lds16(nil, OOB, u + (wave * LOADS_K + q) * 1024);
+    for (int q = 0; q < LK; ++q) load_lds16(nil, OOB, u + (wave * LK + q) * 1024);
   }
 };
 
-// N-contiguous operand: this wave's sub-tile of 128 columns (waves 0-3 load
-// sub-tile 0, waves 4-7 sub-tile 1).  Half h (0, 1) of step j covers rows r0
-// = 64 j + 32 h .. r0 + 31; load Q (0 .. LOADS_H - 1), I = LOADS_H w + Q,
-// covers rows r0 + kr .. +3, kr = 4 (I % 8): lane l takes row r0 + kr + l / 16
-// and column 8 ((l % 16) ^ (4 (l / 16))).  The descriptor's base moves to row
-// r0 (64-bit, so lane offsets stay below 32 rows at any K) while its range
-// stays the bound set at the tile's start: every lane's column and row are
-// checked, so valid lanes never reach it.  Lanes of columns past the
-// sub-tile's valid columns get an out-of-range offset; only a half that
-// reaches past the valid k masks rows.
+// N-contiguous operand: this wave's sub-tile of 128 columns (the first half
+// of the loading waves load sub-tile 0, the second half sub-tile 1).  Half h
+// (0, 1) of step j covers rows r0 = 64 j + 32 h .. r0 + 31; load Q (0 ..
+// LH - 1), I = LH w + Q, covers rows r0 + kr .. +3, kr = 4 (I % 8): lane l
+// takes row r0 + kr + l / 16 and column 8 ((l % 16) ^ (4 (l / 16))).  The
+// descriptor's base moves to row r0 (64-bit, so lane offsets stay below 32
+// rows at any K) while its range stays the bound set at the tile's start:
+// every lane's column and row are checked, so valid lanes never reach it.
+// Lanes of columns past the sub-tile's valid columns get an out-of-range
+// offset; only a half that reaches past the valid k masks rows.
+template <int NL>
 struct NStream {
-  uint64_t base;           // byte address of the sub-tile's row 0
-  uint32_t range, ld;      // descriptor range from row 0; row pitch in bytes
-  uint32_t voff[LOADS_H];  // lane offset of load Q from the half's first row
+  static constexpr int LH = HALF / 1024 / NL;  // 16-byte direct loads per lane and half step
+  uint64_t base;       // byte address of the sub-tile's row 0
+  uint32_t range, ld;  // descriptor range from row 0; row pitch in bytes
+  uint32_t voff[LH];   // lane offset of load Q from the half's first row
   int kmax;
   __device__ __forceinline__ void setup(const NOperand& op, int wave, int lane) {
-    const int sub = (wave * LOADS_H) >> 3;
+    const int sub = (wave * LH) >> 3;
     const i32x4 r = make_rsrc(sub ? op.ptr1 : op.ptr0, sub ? op.range1 : op.range0);
     base = (static_cast<uint64_t>(static_cast<uint32_t>(r[1]) & 0xffffu) << 32) |
            static_cast<uint32_t>(r[0]);
@@ -325,15 +333,15 @@ struct NStream {
     const int col = ((lane & 15) ^ (4 * kl)) * 8;
     const int cols = sub ? op.cols1 : op.cols0;
 #pragma unroll
-    for (int q = 0; q < LOADS_H; ++q) {
-      const int kr = ((wave * LOADS_H + q) & 7) * 4;
+    for (int q = 0; q < LH; ++q) {
+      const int kr = ((wave * LH + q) & 7) * 4;
       voff[q] = col < cols ? static_cast<uint32_t>(kr + kl) * ld + static_cast<uint32_t>(col * 2)
                            : OOB;
     }
   }
   // half h of step j into the LDS half at `u` (both sub-tiles' halves)
   __device__ __forceinline__ void issue(int j, int h, uint32_t u, int wave) const {
-    const int sub = (wave * LOADS_H) >> 3;
+    const int sub = (wave * LH) >> 3;
     const int r0 = j * BK + h * (BK / 2);
     const uint64_t a = base + static_cast<uint64_t>(static_cast<uint32_t>(r0)) * ld;
     i32x4 rs;
@@ -344,15 +352,15 @@ struct NStream {
     const int krem = kmax - r0;
     if (krem >= BK / 2) {
 #pragma unroll
-      for (int q = 0; q < LOADS_H; ++q) {
-        const int I = wave * LOADS_H + q;
+      for (int q = 0; q < LH; ++q) {
+        const int I = wave * LH + q;
         load_lds16(rs, voff[q], u + sub * (HALF / 2) + (I & 7) * 1024);
       }
     } else {
       const int kl = opaque(static_cast<int>(threadIdx.x & 63)) >> 4;
 #pragma unroll
-      for (int q = 0; q < LOADS_H; ++q) {
-        const int I = wave * LOADS_H + q;
+      for (int q = 0; q < LH; ++q) {
+        const int I = wave * LH + q;
         const int kr = (I & 7) * 4;
         load_lds16(rs, kl < krem - kr ? voff[q] : OOB, u + sub * (HALF / 2) + (I & 7) * 1024);
       }
@@ -360,8 +368,8 @@ struct NStream {
   }
   static __device__ __forceinline__ void none(const i32x4& nil, uint32_t u, int wave) {
 #pragma unroll
-    for (int q = 0; q < LOADS_H; ++q) {
-      const int I = wave * LOADS_H + q;
+    for (int q = 0; q < LH; ++q) {
+      const int I = wave * LH + q;
       load_lds16(nil, OOB, u + (I >> 3) * (HALF / 2) + (I & 7) * 1024);
     }
   }
@@ -967,7 +975,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
             static_for<2>([&](auto J) {
               static_for<16>([&](auto R) {
                 constexpr int j = J, r = R;
-                if (32 * j + 8 * (r / 4) + (r % 4) == want) val = acc[i][j][r];
+                // a sum of selects (one term matches): the compiler keeps
+                // it in registers instead of indexing the accumulators
+                val += 32 * j + 8 * (r / 4) + (r % 4) == want ? acc[i][j][r] : 0.0f;
               });
             });
             g.yt[row] = val;
@@ -1105,316 +1115,544 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     }
   };
 
-  // ------------------------------------------------------------ LDS rings
-  // NA = 2 slots of UNIT bytes for operand A, then NB = 3 for operand B, one
-  // K step per slot.  A (called F below) is loaded one step ahead, B (S) two:
-  // in the forward and data-gradient GEMMs B is the expert weights, whose
-  // tiles miss L2 more often; in the weight gradients B is dH (the reverse
-  // order measured 5 % slower there).  The single sync of step s (after its
-  // last fragment reads) waits for step s + 1, then prepares F for step s + 2
-  // and S for step s + 3, into the slots step s has freed (an N-contiguous
-  // operand as two halves of 32 k).  These loads go out between the eight
-  // MFMAs that follow the sync, F's first, so the matrix cores have work
-  // while they are issued and the issue state is never held across
-  // sub-steps (holding it across the whole step costs scalar-register
-  // spills and a branch per load).
-  constexpr bool A_K = !A_N, B_N = !B_K;
-  constexpr int NA = 2, NB = NRING - NA;
-  constexpr int LA = A_K ? LOADS_K : 2 * LOADS_H;  // loads per wave of one step's issue
-  constexpr int LB = B_K ? LOADS_K : 2 * LOADS_H;
-  // At the sync of step s the loads issued after the last of F(s + 1) (the
-  // later of the two operands it needs) are S(s + 2)'s four: the
-  // vector-memory count it may leave.
-  constexpr int X_END = 4;
-  static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
-  static_assert(LA == 4 && LB == 4 && NA == 2 && NB == 3,
-                "the sync count assumes this ring");
-
-  lds_char* const ring = (lds_char*)(lds);  // address-space cast
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
-  struct Frags {
-    bf16x8 a[4], b[2];
-  };
-  // fragments of sub-step `sub` (16 k, 0..3) of the step held in A's ring
-  // slot `sa` and B's ring slot `sb`
-  auto load_frags = [&](Frags& F, int sa, int sb, int sub) __attribute__((always_inline)) {
-    const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
-    const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if constexpr (A_N) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
-      else F.a[i] = AOp::frag(ta, arow[i] + l32, sub, lh);
-    }
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      if constexpr (B_K) F.b[jj] = BOp::frag(tb, brow[jj] + l32, sub, lh);
-      else F.b[jj] = BOp::frag(tb, brow[jj], sub & 1, lane);
-    }
-  };
-  // one fragment f of sub-step `sub` (f = 0..3: A's row blocks, 4..5: B's)
-  auto load_frag1 = [&](Frags& F, int sa, int sb, int sub, auto FI) __attribute__((always_inline)) {
-    constexpr int f = FI;
-    if constexpr (f < 4) {
-      const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
-      if constexpr (A_N) F.a[f] = AOp::frag(ta, arow[f], sub & 1, lane);
-      else F.a[f] = AOp::frag(ta, arow[f] + l32, sub, lh);
-    } else {
-      const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
-      if constexpr (B_K) F.b[f - 4] = BOp::frag(tb, brow[f - 4] + l32, sub, lh);
-      else F.b[f - 4] = BOp::frag(tb, brow[f - 4], sub & 1, lane);
-    }
-  };
-  auto mma = [&](const Frags& F) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj)
-        acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[jj], F.a[i], acc[i][jj], 0, 0, 0);
-  };
-
-  // ---------------------------------------------------------- tile stream
-  // Tiles run one after another, each with its own K loop; A is loaded one
-  // step and B two steps ahead of the sync that needs them.  Near a tile's
-  // end those loads fetch the next tile's first steps (its load streams are
-  // prepared when the current tile starts).  A load that would reach still
-  // further (the next tile has fewer steps than the look-ahead) is issued
-  // out of range into its slot, so every sync's count stays exact, and is
-  // issued again for real when its tile starts, after a full wait.  After a
-  // tile's last step, B's slot of that step holds the epilogue patches; its
-  // refill waits for the epilogue.
-  using AStream = typename std::conditional<A_N, NStream, KStream<MODE == DGRAD_GATE_UP>>::type;
-  using BStream = typename std::conditional<B_N, NStream, KStream<MODE == DGRAD_GATE_UP>>::type;
   const Tables tb{g.mt_start, g.offsets, g.wk_start, g.nz_start};
-  const i32x4 nil = make_rsrc(nullptr, 0);
-  TileIter<MODE> it;
-  it.init(g, tb);
-  zero_acc();
-  Tile tc = it.next(g, tb);
-  if (tc.valid) {
-    AStream sa, xa;  // loads of this tile and of the next one
-    BStream sb, xb;
-    auto prep = [&](const Tile& t, AStream& a, BStream& b) __attribute__((always_inline)) {
-      AOp ao;
-      setupA(t, ao);
-      a.setup(ao, w, lane);
-      BOp bo;
-      setupB(t, bo);
-      b.setup(bo, w, lane);
-    };
-    // part p (0, 1) of one step's loads of an operand into ring slot `slot`:
-    // the two halves of an N-contiguous step; a K-contiguous step at p = 0
-    auto issA = [&](const AStream& st, int j, int slot, int p) __attribute__((always_inline)) {
-      const uint32_t u = lds0 + slot * UNIT;
-      if constexpr (A_N) st.issue(j, p, u + p * HALF, w);
-      else if (p == 0) st.issue(j, u, w);
-    };
-    auto noneA = [&](int slot, int p) __attribute__((always_inline)) {
-      const uint32_t u = lds0 + slot * UNIT;
-      if constexpr (A_N) NStream::none(nil, u + p * HALF, w);
-      else if (p == 0) KStream<false>::none(nil, u, w);
-    };
-    auto issB = [&](const BStream& st, int j, int slot, int p) __attribute__((always_inline)) {
-      const uint32_t u = lds0 + (NA + slot) * UNIT;
-      if constexpr (B_N) st.issue(j, p, u + p * HALF, w);
-      else if (p == 0) st.issue(j, u, w);
-    };
-    auto noneB = [&](int slot, int p) __attribute__((always_inline)) {
-      const uint32_t u = lds0 + (NA + slot) * UNIT;
-      if constexpr (B_N) NStream::none(nil, u + p * HALF, w);
-      else if (p == 0) KStream<false>::none(nil, u, w);
-    };
-
-    prep(tc, sa, sb);
-    // prologue: the loads the syncs of steps -3, -2, -1 would have issued
-    // (B 0; A 0, B 1; A 1, B 2), steps past the tile out of range
-    {
-      const int nk = tc.nk;
-      auto pa = [&](int j) {
-        static_for<2>([&](auto P) {
-          if (j < nk) issA(sa, j, j, P); else noneA(j, P);
+  // The weight gradients (grouped, and the vocabulary's dW) store both
+  // operands with the output index contiguous and read every fragment with
+  // two transposing LDS reads.  When their tiles are long (at least 16 K
+  // steps on average) they run the ping-pong schedule below, which keeps
+  // those reads out of the MFMA stream; its tile change costs an extra
+  // phase, so short tiles, the router's dW (short token chunks) and every
+  // other mode run the single-barrier schedule after it.  The choice is
+  // uniform over the launch.
+  constexpr bool PP_OK = A_N && !B_K && MODE != RT_DW;
+  bool use_pp = false;
+  if constexpr (PP_OK) {
+    if constexpr (DENSE) use_pp = g.kspan >= 16 * BK;
+    else use_pp = 16 * tb.nz(g.E_loc) <= tb.wk(g.E_loc);
+  }
+  if (use_pp) {
+    if constexpr (PP_OK) {
+      // ---------------------------------------------------------- LDS ring
+      // NA = 2 slots of UNIT bytes for operand A (loaded one step ahead), then
+      // 3 for operand B (two steps ahead).
+      constexpr int NA = 2;
+      using St = NStream<4>;
+      static_assert(NRING - NA == 3 && 2 * St::LH == 8, "the wait counts below assume this ring");
+      lds_char* const ring = (lds_char*)(lds);  // address-space cast
+      const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
+      struct Frags {
+        bf16x8 a[4], b[2];
+      };
+      // fragments of sub-step `sub` (16 k, 0..3) of the step held in A's ring
+      // slot `sa` and B's ring slot `sb`
+      auto load_frags = [&](Frags& F, int sa, int sb, int sub) __attribute__((always_inline)) {
+        const lds_char* ta = ring + sa * UNIT + (sub >> 1) * HALF;
+        const lds_char* tbl = ring + (NA + sb) * UNIT + (sub >> 1) * HALF;
+  #pragma unroll
+        for (int i = 0; i < 4; ++i) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
+  #pragma unroll
+        for (int jj = 0; jj < 2; ++jj) F.b[jj] = BOp::frag(tbl, brow[jj], sub & 1, lane);
+      };
+      // the 8 MFMAs of one sub-step, kept in this order and apart from any
+      // other instruction
+      auto mma = [&](const Frags& F) __attribute__((always_inline)) {
+        static_for<8>([&](auto T) {
+          constexpr int t = T;
+          acc[t / 2][t % 2] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
         });
       };
-      auto pb = [&](int j) {
-        static_for<2>([&](auto P) {
-          if (j < nk) issB(sb, j, j, P); else noneB(j, P);
-        });
+      // End of a phase: this wave's LDS reads are done, then the workgroup
+      // barrier.  One asm statement, so the compiler moves no memory access
+      // across it.
+      auto phase_end = []() __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
       };
-      pb(0);
-      pa(0);
-      pb(1);
-      pa(1);
-      pb(2);
-    }
-    wait_vmcnt<X_END>();
-    lgkm_drained();
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
 
-    Frags cur, nxt;
-    int ra = 0, rb = 0;  // ring slots (A: 0..1, B: 0..2) of the step being computed
-    load_frags(cur, 0, 0, 0);
-    auto sync = [&]() __attribute__((always_inline)) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
-    };
-    // the 8 MFMAs of one sub-step on F, with the six fragment reads of the
-    // next sub-step (into G) between the first three, in the order the next
-    // sub-step's MFMAs need them (a0 b0 | b1 a1 | a2 a3), so that each has
-    // five or more MFMAs to arrive
-    auto mma_read = [&](const Frags& F, Frags& G, int sa, int sb, int sub) __attribute__((always_inline)) {
-      static_for<8>([&](auto T) {
-        constexpr int t = T;
-        acc[t / 2][t % 2] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (t < 3) {
-          constexpr int f0 = t == 0 ? 0 : t == 1 ? 5 : 2;
-          constexpr int f1 = t == 0 ? 4 : t == 1 ? 1 : 3;
-          load_frag1(G, sa, sb, sub, std::integral_constant<int, f0>{});
-          load_frag1(G, sa, sb, sub, std::integral_constant<int, f1>{});
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      });
-    };
-    // the 8 MFMAs of one sub-step, kept in this order
-    auto mma_seq = [&](const Frags& F) __attribute__((always_inline)) {
-      static_for<8>([&](auto T) {
-        constexpr int t = T;
-        acc[t / 2][t % 2] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      });
-    };
-    while (true) {
-      const int nk = tc.nk;
-      Tile tn;
-      tn.valid = false;
-      int nkn = 0;
-      unsigned done_a = 0, done_b = 0;  // steps of the next tile loaded for real
-      // part p of the A / B loads aimed at tile step j (past nk: the next tile)
-      auto loadA = [&](int j, int slot, int p) __attribute__((always_inline)) {
-        if (j < nk) {
-          issA(sa, j, slot, p);
-        } else if (j - nk < nkn) {
-          issA(xa, j - nk, slot, p);
-          done_a |= 1u << (j - nk);
-        } else {
-          noneA(slot, p);
-        }
-      };
-      auto loadB = [&](int j, int slot, int p) __attribute__((always_inline)) {
-        if (j < nk) {
-          issB(sb, j, slot, p);
-        } else if (j - nk < nkn) {
-          issB(xb, j - nk, slot, p);
-          done_b |= 1u << (j - nk);
-        } else {
-          noneB(slot, p);
-        }
-      };
-      // One K step.  TAIL: its look-ahead loads may reach past the tile
-      // (the next tile or nothing); otherwise they stay inside it.  LAST:
-      // the tile's last step (B's refill waits for the epilogue).
-      auto step = [&](int ks, auto TAIL, auto LAST) __attribute__((always_inline)) {
-        constexpr bool tail = TAIL, last = LAST;
-        const int ra1 = ra ^ 1, rb1 = rb == 2 ? 0 : rb + 1;  // slots of the next step
-        mma_read(cur, nxt, ra, rb, 1);
-        mma_read(nxt, cur, ra, rb, 2);
-        mma_read(cur, nxt, ra, rb, 3);
-        sync();
-        wait_vmcnt<X_END>();
-        __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        // this step's slots are free: A's refill with step ks + 2, B's with
-        // ks + 3 (deferred past the epilogue on the tile's last step)
-        if constexpr (!last) {
-          lgkm_drained();
-          load_frags(cur, ra1, rb1, 0);
-          __builtin_amdgcn_sched_barrier(0);
-          // the 8 MFMAs of sub-step 3 with the loads between them (A's parts
-          // after the second and fourth, B's after the sixth and eighth)
-          static_for<8>([&](auto T) {
-            constexpr int t = T;
-            acc[t / 2][t % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                nxt.b[t % 2], nxt.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            if constexpr (t % 2 == 1) {
-              if constexpr (t < 4) {
-                if constexpr (tail) loadA(ks + 2, ra, t / 2);
-                else issA(sa, ks + 2, ra, t / 2);
-              } else {
-                if constexpr (tail) loadB(ks + 3, rb, t / 2 - 2);
-                else issB(sb, ks + 3, rb, t / 2 - 2);
-              }
-              __builtin_amdgcn_sched_barrier(0);
-            }
-          });
-          lgkm_drained();
-        } else {
-          loadA(ks + 2, ra, 0);
-          loadA(ks + 2, ra, 1);
-          __builtin_amdgcn_sched_barrier(0);
-          mma(nxt);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        ra = ra1;
-        rb = rb1;
-      };
-      int ks = 0;
-      // steps whose loads stay inside the tile
-      for (; ks + NB < nk; ++ks) step(ks, std::false_type{}, std::false_type{});
-      // the last steps reach into the next tile: prepare its loads now
-      tn = it.next(g, tb);
-      if (tn.valid) {
-        prep(tn, xa, xb);
-        nkn = tn.nk;
-      }
-      for (; ks + 1 < nk; ++ks) step(ks, std::true_type{}, std::false_type{});
-      step(ks, std::true_type{}, std::true_type{});
-      // epilogue patches: B's slot of the tile's last step
-      const int rlast = rb == 0 ? 2 : rb - 1;
-      lds_char* const patch = ring + (NA + rlast) * UNIT + w * PATCH_BYTES;
-      epilogue(tc, patch);
-      zero_acc();
-      // the patch reads are done once the LDS counter drains; the stores stay
-      // in flight (the next sync's vector-memory wait covers them, in order)
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      __builtin_amdgcn_s_barrier();  // every wave is done with its patch
-      __builtin_amdgcn_sched_barrier(0);
-      if (!tn.valid) break;
-      // B's deferred refill (tile step nk + 2 = the next tile's step 2)
-      loadB(nk + 2, rlast, 0);
-      loadB(nk + 2, rlast, 1);
-      tc = tn;
-      sa = xa;
-      sb = xb;
-      // Steps of the new tile that a shorter tile before it could not load
-      // ahead went out as out-of-range loads: issue them now into their
-      // slots and wait for every load (rare: only after tiles of fewer
-      // steps than the look-ahead).
-      const unsigned need_a = (1u << min(tc.nk, NA)) - 1u, need_b = (1u << min(tc.nk, NB)) - 1u;
-      if ((done_a & need_a) != need_a || (done_b & need_b) != need_b) {
-        for (int j = 0; j < min(tc.nk, NA); ++j)
-          if (!((done_a >> j) & 1u)) {
-            const int sl = (ra + j) & 1;
-            issA(sa, j, sl, 0);
-            issA(sa, j, sl, 1);
+      // -------------------------------------------------------- tile stream
+      // Waves 0-3 (group 0, one per SIMD) and waves 4-7 (group 1) each hold
+      // half of the tile's B-side columns.  Time runs in phases separated by
+      // workgroup barriers.  In a memory phase a group issues its operand
+      // loads and reads the fragments of one half step (two sub-steps) from
+      // LDS; in the compute phase that follows it runs that half step's 16
+      // MFMAs per wave and nothing else.  Group 1 runs one phase behind group
+      // 0, so on every SIMD one wave issues MFMAs while the other moves data.
+      // Every wave passes the same number of barriers: two per half step, one
+      // between consecutive tiles, and one more at the start (group 1: the
+      // stagger) or at the end (group 0: its wait before the last epilogue).
+      //   Group 0 loads all of operand A (each wave a quarter of a step), step
+      // j + 1 at the start of step j into the slot step j - 1 freed; its wait
+      // for it closes step j.  Group 1 loads all of operand B, step j + 2 at
+      // the start of step j; its wait for step j + 1 closes its second memory
+      // phase of step j.
+      //   Loads for steps past the current tile fetch the next tile's first
+      // steps (its streams are prepared before the tile's last two steps).  A
+      // B step that would lie beyond the next tile (after a tile of one step)
+      // is issued when its tile becomes the next one, before it is needed.
+      // Between tiles both groups write out the finished tile in one phase
+      // (one more barrier for each); the output patches sit in B's slot of that
+      // tile's last step, so its refill (step 2 of the new tile) waits for
+      // group 1's second memory phase of the new tile.
+      const int grp = w >> 2, wq = w & 3;
+      auto run = [&](auto GC) __attribute__((always_inline)) {
+        constexpr int G = GC;
+        TileIter<MODE> it;
+        it.init(g, tb);
+        Tile tc = it.next(g, tb);
+        if (!tc.valid) return;
+        St cur, nxt;  // this group's loads of the current and of the next tile
+        auto prep = [&](const Tile& t, St& st) __attribute__((always_inline)) {
+          if constexpr (G == 0) {
+            AOp o;
+            setupA(t, o);
+            st.setup(o, wq, lane);
+          } else {
+            BOp o;
+            setupB(t, o);
+            st.setup(o, wq, lane);
           }
-        for (int j = 0; j < min(tc.nk, NB); ++j)
-          if (!((done_b >> j) & 1u)) {
-            const int sl = (rb + j) % 3;
-            issB(sb, j, sl, 0);
-            issB(sb, j, sl, 1);
+        };
+        // all of one step's loads of this group's operand into its ring slot
+        auto issue = [&](const St& st, int j, int slot) __attribute__((always_inline)) {
+          const uint32_t u = lds0 + (G == 0 ? slot : NA + slot) * UNIT;
+          st.issue(j, 0, u, wq);
+          st.issue(j, 1, u + HALF, wq);
+        };
+        zero_acc();
+        prep(tc, cur);
+        int ra = 0, rb = 0;  // ring slots (A: 0..1, B: 0..2) of the current step
+        int bl = 0;          // group 1: first B step, counted in the current tile, not yet issued
+        // prologue: A step 0 (group 0), B steps 0 and 1 (group 1)
+        if constexpr (G == 0) {
+          issue(cur, 0, 0);
+        } else {
+          issue(cur, 0, 0);
+          bl = 1;
+          if (tc.nk > 1) {
+            issue(cur, 1, 1);
+            bl = 2;
           }
+        }
         wait_vmcnt<0>();
-        __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      lgkm_drained();
-      load_frags(cur, ra, rb, 0);
+        phase_end();
+        if constexpr (G == 1) phase_end();
+
+        Frags F0, F1;
+        Tile tp;  // the tile written out at the start of the next one
+        bool has_prev = false;
+        while (true) {
+          if (has_prev) {
+            // The previous tile's outputs, through patches in B's slot of its
+            // last step, both groups in one phase: group 0 first waits out
+            // group 1's last half step, and group 1 starts its first memory
+            // phase of the new tile one phase later (group 0's runs beside the
+            // epilogues).
+            if constexpr (G == 0) phase_end();
+            lgkm_drained();
+            epilogue(tp, ring + (NA + (rb == 0 ? 2 : rb - 1)) * UNIT + w * PATCH_BYTES);
+            zero_acc();
+            if constexpr (G == 1) {
+              if (tc.valid) phase_end();
+            }
+          }
+          if (!tc.valid) break;
+          const int nk = tc.nk;
+          int nkn = 0;  // steps of the next tile (0: none)
+          // step j counted in the current tile (past nk: the next tile's) into
+          // `slot`, if its tile is the current or the next one
+          auto issue_at = [&](int j, int slot) __attribute__((always_inline)) {
+            if (j < nk) {
+              issue(cur, j, slot);
+              return true;
+            }
+            if (j - nk < nkn) {
+              issue(nxt, j - nk, slot);
+              return true;
+            }
+            return false;
+          };
+          // One K step: two half steps, each a memory and a compute phase.
+          // TAIL: its loads may reach past the tile (the next one or nothing).
+          auto step = [&](int s, auto TAILC) __attribute__((always_inline)) {
+            constexpr bool TAIL = TAILC;
+            bool b8 = false;  // group 1: this step issued B step s + 2 (the last of its loads)
+            // ---- memory phase, first half
+            if constexpr (G == 0) {
+              if constexpr (TAIL) issue_at(s + 1, ra ^ 1);
+              else issue(cur, s + 1, ra ^ 1);
+            } else {
+              // B up to step s + 2; at a tile's first step only up to step 1
+              // (step 2 goes to the slot that held the output patches)
+              const int tgt = s == 0 ? 1 : s + 2;
+              while (bl <= tgt) {
+                const int d3 = rb + bl - s;  // 0 .. 4
+                const int slot = d3 >= 3 ? d3 - 3 : d3;
+                if constexpr (TAIL) {
+                  if (!issue_at(bl, slot)) break;
+                } else {
+                  issue(cur, bl, slot);
+                }
+                ++bl;
+              }
+              b8 = s != 0 && bl == s + 3;
+            }
+            lgkm_drained();
+            load_frags(F0, ra, rb, 0);
+            load_frags(F1, ra, rb, 1);
+            phase_end();
+            // ---- compute phase, first half
+            mma(F0);
+            mma(F1);
+            phase_end();
+            // ---- memory phase, second half
+            if constexpr (G == 1) {
+              if (s == 0 && bl == 2) {
+                if (issue_at(2, rb == 0 ? 2 : rb - 1)) {
+                  bl = 3;
+                  b8 = true;
+                }
+              }
+            }
+            load_frags(F0, ra, rb, 2);
+            load_frags(F1, ra, rb, 3);
+            if constexpr (G == 1) {
+              // B step s + 1 has landed (step s + 2, issued after it, may still
+              // be in flight)
+              if (b8) wait_vmcnt<8>();
+              else wait_vmcnt<0>();
+            }
+            phase_end();
+            // ---- compute phase, second half
+            mma(F0);
+            mma(F1);
+            if constexpr (G == 0) wait_vmcnt<0>();  // A step s + 1 has landed
+            phase_end();
+            ra ^= 1;
+            rb = rb == 2 ? 0 : rb + 1;
+          };
+          int s = 0;
+          for (; s + 2 < nk; ++s) step(s, std::false_type{});
+          // the last two steps load into the next tile: prepare its streams
+          const Tile tn = it.next(g, tb);
+          if (tn.valid) {
+            prep(tn, nxt);
+            nkn = tn.nk;
+          }
+          for (; s < nk; ++s) step(s, std::true_type{});
+          tp = tc;
+          has_prev = true;
+          tc = tn;
+          cur = nxt;
+          if constexpr (G == 1) bl -= nk;
+        }
+        wait_vmcnt<0>();
+      };
+      if (grp == 0) run(std::integral_constant<int, 0>{});
+      else run(std::integral_constant<int, 1>{});
     }
-    // the last steps' out-of-range loads still write their (zero) slots:
-    // let them land before the workgroup's LDS is released
-    wait_vmcnt<0>();
+  } else {
+    // ------------------------------------------------------------ LDS rings
+    // NA = 2 slots of UNIT bytes for operand A, then NB = 3 for operand B, one
+    // K step per slot.  A (called F below) is loaded one step ahead, B (S) two:
+    // in the forward and data-gradient GEMMs B is the expert weights, whose
+    // tiles miss L2 more often; in the weight gradients B is dH (the reverse
+    // order measured 5 % slower there).  The single sync of step s (after its
+    // last fragment reads) waits for step s + 1, then prepares F for step s + 2
+    // and S for step s + 3, into the slots step s has freed (an N-contiguous
+    // operand as two halves of 32 k).  These loads go out between the eight
+    // MFMAs that follow the sync, F's first, so the matrix cores have work
+    // while they are issued and the issue state is never held across
+    // sub-steps (holding it across the whole step costs scalar-register
+    // spills and a branch per load).
+    constexpr bool A_K = !A_N, B_N = !B_K;
+    constexpr int NA = 2, NB = NRING - NA;
+    constexpr int LA = A_K ? KStream<false, NWAVE>::LK : 2 * NStream<NWAVE>::LH;  // loads per wave of one step's issue
+    constexpr int LB = B_K ? KStream<false, NWAVE>::LK : 2 * NStream<NWAVE>::LH;
+    // At the sync of step s the loads issued after the last of F(s + 1) (the
+    // later of the two operands it needs) are S(s + 2)'s four: the
+    // vector-memory count it may leave.
+    constexpr int X_END = 4;
+    static_assert(!(A_N && B_K), "no mode has an N-contiguous A with a K-contiguous B");
+    static_assert(LA == 4 && LB == 4 && NA == 2 && NB == 3,
+                  "the sync count assumes this ring");
+
+    lds_char* const ring = (lds_char*)(lds);  // address-space cast
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
+    struct Frags {
+      bf16x8 a[4], b[2];
+    };
+    // fragments of sub-step `sub` (16 k, 0..3) of the step held in A's ring
+    // slot `sa` and B's ring slot `sb`
+    auto load_frags = [&](Frags& F, int sa, int sb, int sub) __attribute__((always_inline)) {
+      const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
+      const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
+  #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (A_N) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
+        else F.a[i] = AOp::frag(ta, arow[i] + l32, sub, lh);
+      }
+  #pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        if constexpr (B_K) F.b[jj] = BOp::frag(tb, brow[jj] + l32, sub, lh);
+        else F.b[jj] = BOp::frag(tb, brow[jj], sub & 1, lane);
+      }
+    };
+    // one fragment f of sub-step `sub` (f = 0..3: A's row blocks, 4..5: B's)
+    auto load_frag1 = [&](Frags& F, int sa, int sb, int sub, auto FI) __attribute__((always_inline)) {
+      constexpr int f = FI;
+      if constexpr (f < 4) {
+        const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
+        if constexpr (A_N) F.a[f] = AOp::frag(ta, arow[f], sub & 1, lane);
+        else F.a[f] = AOp::frag(ta, arow[f] + l32, sub, lh);
+      } else {
+        const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
+        if constexpr (B_K) F.b[f - 4] = BOp::frag(tb, brow[f - 4] + l32, sub, lh);
+        else F.b[f - 4] = BOp::frag(tb, brow[f - 4], sub & 1, lane);
+      }
+    };
+    auto mma = [&](const Frags& F) __attribute__((always_inline)) {
+  #pragma unroll
+      for (int i = 0; i < 4; ++i)
+  #pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+          acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[jj], F.a[i], acc[i][jj], 0, 0, 0);
+    };
+
+    // ---------------------------------------------------------- tile stream
+    // Tiles run one after another, each with its own K loop; A is loaded one
+    // step and B two steps ahead of the sync that needs them.  Near a tile's
+    // end those loads fetch the next tile's first steps (its load streams are
+    // prepared when the current tile starts).  A load that would reach still
+    // further (the next tile has fewer steps than the look-ahead) is issued
+    // out of range into its slot, so every sync's count stays exact, and is
+    // issued again for real when its tile starts, after a full wait.  After a
+    // tile's last step, B's slot of that step holds the epilogue patches; its
+    // refill waits for the epilogue.
+    using AStream = typename std::conditional<A_N, NStream<NWAVE>, KStream<MODE == DGRAD_GATE_UP, NWAVE>>::type;
+    using BStream = typename std::conditional<B_N, NStream<NWAVE>, KStream<MODE == DGRAD_GATE_UP, NWAVE>>::type;
+    const i32x4 nil = make_rsrc(nullptr, 0);
+    TileIter<MODE> it;
+    it.init(g, tb);
+    zero_acc();
+    Tile tc = it.next(g, tb);
+    if (tc.valid) {
+      AStream sa, xa;  // loads of this tile and of the next one
+      BStream sb, xb;
+      auto prep = [&](const Tile& t, AStream& a, BStream& b) __attribute__((always_inline)) {
+        AOp ao;
+        setupA(t, ao);
+        a.setup(ao, w, lane);
+        BOp bo;
+        setupB(t, bo);
+        b.setup(bo, w, lane);
+      };
+      // part p (0, 1) of one step's loads of an operand into ring slot `slot`:
+      // the two halves of an N-contiguous step; a K-contiguous step at p = 0
+      auto issA = [&](const AStream& st, int j, int slot, int p) __attribute__((always_inline)) {
+        const uint32_t u = lds0 + slot * UNIT;
+        if constexpr (A_N) st.issue(j, p, u + p * HALF, w);
+        else if (p == 0) st.issue(j, u, w);
+      };
+      auto noneA = [&](int slot, int p) __attribute__((always_inline)) {
+        const uint32_t u = lds0 + slot * UNIT;
+        if constexpr (A_N) NStream<NWAVE>::none(nil, u + p * HALF, w);
+        else if (p == 0) KStream<false, NWAVE>::none(nil, u, w);
+      };
+      auto issB = [&](const BStream& st, int j, int slot, int p) __attribute__((always_inline)) {
+        const uint32_t u = lds0 + (NA + slot) * UNIT;
+        if constexpr (B_N) st.issue(j, p, u + p * HALF, w);
+        else if (p == 0) st.issue(j, u, w);
+      };
+      auto noneB = [&](int slot, int p) __attribute__((always_inline)) {
+        const uint32_t u = lds0 + (NA + slot) * UNIT;
+        if constexpr (B_N) NStream<NWAVE>::none(nil, u + p * HALF, w);
+        else if (p == 0) KStream<false, NWAVE>::none(nil, u, w);
+      };
+
+      prep(tc, sa, sb);
+      // prologue: the loads the syncs of steps -3, -2, -1 would have issued
+      // (B 0; A 0, B 1; A 1, B 2), steps past the tile out of range
+      {
+        const int nk = tc.nk;
+        auto pa = [&](int j) {
+          static_for<2>([&](auto P) {
+            if (j < nk) issA(sa, j, j, P); else noneA(j, P);
+          });
+        };
+        auto pb = [&](int j) {
+          static_for<2>([&](auto P) {
+            if (j < nk) issB(sb, j, j, P); else noneB(j, P);
+          });
+        };
+        pb(0);
+        pa(0);
+        pb(1);
+        pa(1);
+        pb(2);
+      }
+      wait_vmcnt<X_END>();
+      lgkm_drained();
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+
+      Frags cur, nxt;
+      int ra = 0, rb = 0;  // ring slots (A: 0..1, B: 0..2) of the step being computed
+      load_frags(cur, 0, 0, 0);
+      auto sync = [&]() __attribute__((always_inline)) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's fragment reads are done
+      };
+      // the 8 MFMAs of one sub-step on F, with the six fragment reads of the
+      // next sub-step (into G) between the first three, in the order the next
+      // sub-step's MFMAs need them (a0 b0 | b1 a1 | a2 a3), so that each has
+      // five or more MFMAs to arrive
+      auto mma_read = [&](const Frags& F, Frags& G, int sa, int sb, int sub) __attribute__((always_inline)) {
+        static_for<8>([&](auto T) {
+          constexpr int t = T;
+          acc[t / 2][t % 2] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[t % 2], F.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          if constexpr (t < 6) {
+            constexpr int f0 = t == 0 ? 0 : t == 1 ? 4 : t == 2 ? 5 : t == 3 ? 1 : t == 4 ? 2 : 3;
+            load_frag1(G, sa, sb, sub, std::integral_constant<int, f0>{});
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        });
+      };
+      while (true) {
+        const int nk = tc.nk;
+        Tile tn;
+        tn.valid = false;
+        int nkn = 0;
+        unsigned done_a = 0, done_b = 0;  // steps of the next tile loaded for real
+        // part p of the A / B loads aimed at tile step j (past nk: the next tile)
+        auto loadA = [&](int j, int slot, int p) __attribute__((always_inline)) {
+          if (j < nk) {
+            issA(sa, j, slot, p);
+          } else if (j - nk < nkn) {
+            issA(xa, j - nk, slot, p);
+            done_a |= 1u << (j - nk);
+          } else {
+            noneA(slot, p);
+          }
+        };
+        auto loadB = [&](int j, int slot, int p) __attribute__((always_inline)) {
+          if (j < nk) {
+            issB(sb, j, slot, p);
+          } else if (j - nk < nkn) {
+            issB(xb, j - nk, slot, p);
+            done_b |= 1u << (j - nk);
+          } else {
+            noneB(slot, p);
+          }
+        };
+        // One K step.  TAIL: its look-ahead loads may reach past the tile
+        // (the next tile or nothing); otherwise they stay inside it.  LAST:
+        // the tile's last step (B's refill waits for the epilogue).
+        auto step = [&](int ks, auto TAIL, auto LAST) __attribute__((always_inline)) {
+          constexpr bool tail = TAIL, last = LAST;
+          const int ra1 = ra ^ 1, rb1 = rb == 2 ? 0 : rb + 1;  // slots of the next step
+          mma_read(cur, nxt, ra, rb, 1);
+          mma_read(nxt, cur, ra, rb, 2);
+          mma_read(cur, nxt, ra, rb, 3);
+          sync();
+          wait_vmcnt<X_END>();
+          __builtin_amdgcn_s_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+          // this step's slots are free: A's refill with step ks + 2, B's with
+          // ks + 3 (deferred past the epilogue on the tile's last step)
+          if constexpr (!last) {
+            lgkm_drained();
+            load_frags(cur, ra1, rb1, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            // the 8 MFMAs of sub-step 3 with the loads between them (A's parts
+            // after the second and fourth, B's after the sixth and eighth)
+            static_for<8>([&](auto T) {
+              constexpr int t = T;
+              acc[t / 2][t % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  nxt.b[t % 2], nxt.a[t / 2], acc[t / 2][t % 2], 0, 0, 0);
+              __builtin_amdgcn_sched_barrier(0);
+              if constexpr (t % 2 == 1) {
+                if constexpr (t < 4) {
+                  if constexpr (tail) loadA(ks + 2, ra, t / 2);
+                  else issA(sa, ks + 2, ra, t / 2);
+                } else {
+                  if constexpr (tail) loadB(ks + 3, rb, t / 2 - 2);
+                  else issB(sb, ks + 3, rb, t / 2 - 2);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            });
+            lgkm_drained();
+          } else {
+            loadA(ks + 2, ra, 0);
+            loadA(ks + 2, ra, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(nxt);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          ra = ra1;
+          rb = rb1;
+        };
+        int ks = 0;
+        // steps whose loads stay inside the tile
+        for (; ks + NB < nk; ++ks) step(ks, std::false_type{}, std::false_type{});
+        // the last steps reach into the next tile: prepare its loads now
+        tn = it.next(g, tb);
+        if (tn.valid) {
+          prep(tn, xa, xb);
+          nkn = tn.nk;
+        }
+        for (; ks + 1 < nk; ++ks) step(ks, std::true_type{}, std::false_type{});
+        step(ks, std::true_type{}, std::true_type{});
+        // epilogue patches: B's slot of the tile's last step
+        const int rlast = rb == 0 ? 2 : rb - 1;
+        lds_char* const patch = ring + (NA + rlast) * UNIT + w * PATCH_BYTES;
+        epilogue(tc, patch);
+        zero_acc();
+        // the patch reads are done once the LDS counter drains; the stores stay
+        // in flight (the next sync's vector-memory wait covers them, in order)
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();  // every wave is done with its patch
+        __builtin_amdgcn_sched_barrier(0);
+        if (!tn.valid) break;
+        // B's deferred refill (tile step nk + 2 = the next tile's step 2)
+        loadB(nk + 2, rlast, 0);
+        loadB(nk + 2, rlast, 1);
+        tc = tn;
+        sa = xa;
+        sb = xb;
+        // Steps of the new tile that a shorter tile before it could not load
+        // ahead went out as out-of-range loads: issue them now into their
+        // slots and wait for every load (rare: only after tiles of fewer
+        // steps than the look-ahead).
+        const unsigned need_a = (1u << min(tc.nk, NA)) - 1u, need_b = (1u << min(tc.nk, NB)) - 1u;
+        if ((done_a & need_a) != need_a || (done_b & need_b) != need_b) {
+          for (int j = 0; j < min(tc.nk, NA); ++j)
+            if (!((done_a >> j) & 1u)) {
+              const int sl = (ra + j) & 1;
+              issA(sa, j, sl, 0);
+              issA(sa, j, sl, 1);
+            }
+          for (int j = 0; j < min(tc.nk, NB); ++j)
+            if (!((done_b >> j) & 1u)) {
+              const int sl = (rb + j) % 3;
+              issB(sb, j, sl, 0);
+              issB(sb, j, sl, 1);
+            }
+          wait_vmcnt<0>();
+          __builtin_amdgcn_s_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        lgkm_drained();
+        load_frags(cur, ra, rb, 0);
+      }
+      // the last steps' out-of-range loads still write their (zero) slots:
+      // let them land before the workgroup's LDS is released
+      wait_vmcnt<0>();
+    }
   }
   if constexpr (WGRAD) {
     // experts without rows: their weight gradients are exact zeros

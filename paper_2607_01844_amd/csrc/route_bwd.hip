@@ -227,17 +227,39 @@ __global__ __launch_bounds__(256) void route_split_w_kernel(const float* __restr
   split_bf16(w[static_cast<int64_t>(j) * E + e], hi, lo);
   w3[i] = grp == 1 ? lo : hi;
 }
-// bpart[c][e] = sum over the tokens of chunk c, ascending, of dl[t][e]
-__global__ __launch_bounds__(256) void route_dbias_part_kernel(const float* __restrict__ dl,
-                                                               int64_t T, int E, int64_t chunk,
-                                                               float* __restrict__ bpart) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
+// bpart[c][e] = sum over the tokens of chunk c of dl[t][e].  Lane = expert
+// (64 per block); wave w of the block's 16 sums the chunk's tokens t0 + w,
+// t0 + w + 16, ... in ascending order, eight loads in flight, and the 16
+// wave sums are then added in wave order (a fixed order: the result repeats
+// bit for bit).
+constexpr int DB_WAVES = 16;
+__global__ __launch_bounds__(64 * DB_WAVES) void route_dbias_part_kernel(const float* __restrict__ dl,
+                                                                         int64_t T, int E, int64_t chunk,
+                                                                         float* __restrict__ bpart) {
+  __shared__ float red[DB_WAVES][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int e = blockIdx.x * 64 + lane;
   const int c = blockIdx.y;
-  if (e >= E) return;
   const int64_t t0 = c * chunk, t1 = std::min(T, t0 + chunk);
   float acc = 0.0f;
-  for (int64_t t = t0; t < t1; ++t) acc += dl[t * E + e];
-  bpart[static_cast<int64_t>(c) * E + e] = acc;
+  if (e < E) {
+    int64_t t = t0 + wv;
+    for (; t + 7 * DB_WAVES < t1; t += 8 * DB_WAVES) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = dl[(t + u * DB_WAVES) * E + e];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    for (; t < t1; t += DB_WAVES) acc += dl[t * E + e];
+  }
+  red[wv][lane] = acc;
+  __syncthreads();
+  if (wv == 0 && e < E) {
+    float sum = red[0][lane];
+    for (int q = 1; q < DB_WAVES; ++q) sum += red[q][lane];
+    bpart[static_cast<int64_t>(c) * E + e] = sum;
+  }
 }
 
 // dx[t][j] = bf16( [float(dx[t][j]) +] sum over e ascending of dl[t][e] * W_r[j][e] ).
@@ -375,9 +397,9 @@ hipError_t launch_route_bwd_mfma(const uint16_t* x, const float* w, int64_t T, i
                                                                                     ld3, dl3);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   if (dbias != nullptr) {
-    route_dbias_part_kernel<<<dim3(static_cast<unsigned>(ceil_div(E, 256)),
+    route_dbias_part_kernel<<<dim3(static_cast<unsigned>(ceil_div(E, 64)),
                                    static_cast<unsigned>(S)),
-                              256, 0, s>>>(dl, T, E, chunk, bpart);
+                              64 * DB_WAVES, 0, s>>>(dl, T, E, chunk, bpart);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
   prof_end(K_ROUTE_SPLIT, s);

@@ -98,7 +98,16 @@ SMALL = {
     # stream carries its LDS ring and deferred epilogue refill across tile
     # boundaries; about 768 rows per expert, ragged around 3 row tiles
     "tiles_per_cu": W.Workload("tiles_per_cu", T=8192, d=768, E=64, k=6, f=768),
+    # weight gradients on the ping-pong schedule (their tiles average at least
+    # 16 K steps): Zipf(2.3) loads from 1 to 192 K steps per tile, 1.1 to 2.3
+    # tiles per CU, so tiles of one and two steps follow one another and the
+    # B loads that would reach past the next tile are issued late
+    "pp_skew": W.Workload("pp_skew", T=12288, d=1024, E=20, k=2, f=1024, routing="zipf",
+                          zipf_s=2.3, n_empty=2),
 }
+
+# workloads whose weight gradients must take the ping-pong schedule
+PP_CASES = {"pp_skew"}
 
 
 @pytest.mark.parametrize("name", list(SMALL))
@@ -107,6 +116,13 @@ def test_small_full_parity(name):
     _say(f"[parity] {name} {wl.describe()}")
     inp = make(wl)
     gpu = run_layer(inp, wl)
+    if name in PP_CASES:
+        # the kernel's choice: K steps summed over experts with rows at
+        # least 16 per such expert
+        n = np.diff(gpu["expert_offsets"].cpu().numpy().astype(np.int64))
+        steps = (n + 63) // 64
+        assert steps.sum() >= 16 * (n > 0).sum(), (steps.sum(), (n > 0).sum())
+        assert steps[n > 0].min() <= 2, steps
     errs = P.check_full(inp, wl, gpu)
     _say(f"[parity] {name} ok {errs}")
 

@@ -64,6 +64,9 @@ SMALL = [
     # not (V % 8 != 0: W and dW go through padded block copies)
     ("split_k", 300, 136, 3000, [1024, 2048]),
     ("split_k_staged", 300, 136, 3001, [1024]),
+    # a dW product of 1100 contraction rows (at least 16 K steps): the
+    # ping-pong schedule
+    ("long_dw", 1100, 136, 700, [256, 704]),
 ]
 
 
