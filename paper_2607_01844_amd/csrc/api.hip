@@ -144,7 +144,8 @@ MOE_API const char* moe_last_error(void) { return g_last_error.c_str(); }
 MOE_API int moe_route_workspace_bytes(int64_t T, int E, size_t* bytes) {
   const char* fn = "moe_route_workspace_bytes";
   CHECK(bytes != nullptr, "bytes is NULL");
-  CHECK(T >= 0 && E >= 1 && E <= MOE_MAX_E, "bad T or E");
+  CHECK(T >= 0 && T < (int64_t{1} << 31), "T out of [0, 2^31)");
+  CHECK(E >= 1 && E <= MOE_MAX_E, "E out of [1, MOE_MAX_E]");
   *bytes = moe::align_up(sizeof(float) * static_cast<size_t>(T) * E, 256);
   return MOE_OK;
 }
@@ -178,7 +179,8 @@ MOE_API int moe_route(const moe_bf16* x, const float* w_router, const float* rou
 MOE_API int moe_route_bwd_workspace_bytes(int64_t T, int d, int E, size_t* bytes) {
   const char* fn = "moe_route_bwd_workspace_bytes";
   CHECK(bytes != nullptr, "bytes is NULL");
-  CHECK(T >= 0 && E >= 1 && E <= MOE_MAX_E, "bad T or E");
+  CHECK(T >= 0 && T < (int64_t{1} << 31), "T out of [0, 2^31)");
+  CHECK(E >= 1 && E <= MOE_MAX_E, "E out of [1, MOE_MAX_E]");
   if (int r = check_dim(fn, d, "d")) return r;
   *bytes = moe::route_bwd_ws_bytes(T, d, E);
   return MOE_OK;

@@ -7,6 +7,8 @@ import re
 
 import pytest
 
+from tests.abi_cases import INVALID, P, TOO_SMALL, Z
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "moe.h")
 
@@ -65,81 +67,15 @@ def test_workspace_queries(lib):
                                                   ctypes.byref(n)) == 0
     assert n.value - fwd >= 24576 * 1408 * 2 and n.value < 2 * fwd + 4096
     assert lib.moe_route_workspace_bytes(-1, 64, ctypes.byref(n)) == -1
+    # the header's limit T * k < 2^31 bounds T in the router's queries too
+    assert lib.moe_route_workspace_bytes(1 << 31, 64, ctypes.byref(n)) == -1
+    assert lib.moe_route_bwd_workspace_bytes(1 << 31, 64, 8, ctypes.byref(n)) == -1
+    assert lib.moe_route_bwd_workspace_bytes((1 << 31) - 1, 262144, 1024, ctypes.byref(n)) == 0
     assert lib.moe_grouped_swiglu_workspace_bytes(10, 4, 12, 16, 0, ctypes.byref(n)) == -1
 
 
-# Each case breaks exactly one rule; validation must reject it before any
-# HIP call.  Pointers are 16-byte aligned dummies that are never touched.
-P = ctypes.c_void_p(4096)
-MIS = ctypes.c_void_p(4096 + 2)
-Z = None
-
-
 @pytest.mark.skipif(not _no_gpu(), reason="dummy pointers are only safe without a GPU")
-@pytest.mark.parametrize("case", [
-    ("k > E", lambda L: L.moe_route(P, P, Z, 10, 64, 4, 5, 0, P, P, P, Z, 0, Z)),
-    ("k > MAX_K", lambda L: L.moe_route(P, P, Z, 10, 64, 64, 17, 0, P, P, P, Z, 0, Z)),
-    ("E > MAX_E", lambda L: L.moe_route(P, P, Z, 10, 64, 2000, 2, 0, P, P, P, Z, 0, Z)),
-    ("d % 8", lambda L: L.moe_route(P, P, Z, 10, 60, 8, 2, 0, P, P, P, Z, 0, Z)),
-    ("d > MAX_DIM", lambda L: L.moe_route(P, P, Z, 10, 262152, 8, 2, 0, P, P, P, Z, 0, Z)),
-    ("f > MAX_DIM", lambda L: L.moe_grouped_swiglu_fwd(P, P, 4, 100, 8, 262152, P, P, P, P, P,
-                                                       P, P, 1 << 20, Z)),
-    ("renorm", lambda L: L.moe_route(P, P, Z, 10, 64, 8, 2, 2, P, P, P, Z, 0, Z)),
-    ("null x", lambda L: L.moe_route(Z, P, Z, 10, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
-    ("misaligned", lambda L: L.moe_route(MIS, P, Z, 10, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
-    ("T<0", lambda L: L.moe_route(P, P, Z, -1, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
-    ("T*k overflow", lambda L: L.moe_route(P, P, Z, 1 << 30, 64, 8, 2, 0, P, P, P, Z, 0, Z)),
-    ("expert range", lambda L: L.moe_permute(P, P, 10, 64, 8, 2, 6, 3, P, Z, P, P, P, P, 1 << 20,
-                                             Z)),
-    ("num_local 0", lambda L: L.moe_permute(P, P, 10, 64, 8, 2, 0, 0, P, Z, P, P, P, P, 1 << 20,
-                                            Z)),
-    ("f % 8", lambda L: L.moe_grouped_swiglu_fwd(P, P, 4, 100, 64, 36, P, P, P, P, P, P, P,
-                                                 1 << 20, Z)),
-    ("bwd flags 0", lambda L: L.moe_grouped_swiglu_bwd(P, P, P, P, P, 4, 100, 64, 32, P, P, P, P,
-                                                       P, P, P, 0, P, 1 << 20, Z)),
-    ("bwd flags bad", lambda L: L.moe_grouped_swiglu_bwd(P, P, P, P, P, 4, 100, 64, 32, P, P, P,
-                                                         P, P, P, P, 4, P, 1 << 20, Z)),
-    ("wgrad null dw", lambda L: L.moe_grouped_swiglu_bwd(P, P, P, P, P, 4, 100, 64, 32, P, P, P,
-                                                         P, Z, P, P, 2, P, 1 << 20, Z)),
-    ("combine k", lambda L: L.moe_combine(P, P, P, 10, 64, 0, P, Z)),
-    ("combine_bwd d", lambda L: L.moe_combine_bwd(P, P, P, P, 10, 4, 2, P, P, Z)),
-    ("route_bwd renorm", lambda L: L.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 3, P, Z, Z, 1,
-                                                   Z, P, 1 << 20, Z)),
-    ("route_bwd null dw", lambda L: L.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, Z, Z, Z, 1,
-                                                    Z, P, 1 << 20, Z)),
-    ("route_bwd accumulate", lambda L: L.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, P, Z, P,
-                                                       2, Z, P, 1 << 20, Z)),
-    ("chunked chunk 0", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 32, P, P, P,
-                                                        0, P, P, 1 << 20, Z, Z)),
-    ("chunked range", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 4, 8, 32, P, P, P, 4,
-                                                      P, P, 1 << 20, Z, Z)),
-    ("chunked f % 8", lambda L: L.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 30, P, P, P, 4,
-                                                      P, P, 1 << 20, Z, Z)),
-    ("vocab vblock % 8", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 12, P, P, P, 1 << 30,
-                                                        Z)),
-    ("vocab H % 8", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 60, 100, 16, P, P, P, 1 << 30, Z)),
-    ("vocab V 0", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 64, 0, 16, P, P, P, 1 << 30, Z)),
-    ("vocab N<0", lambda L: L.moe_vocab_loss_fwd(P, P, P, -1, 64, 100, 16, P, P, P, 1 << 30, Z)),
-    ("vocab null lse", lambda L: L.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 16, P, Z, P, 1 << 30,
-                                                      Z)),
-    ("vocab bwd null dw", lambda L: L.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, P, Z, P,
-                                                         1 << 30, Z)),
-    ("vocab bwd misaligned dx", lambda L: L.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, MIS,
-                                                               P, P, 1 << 30, Z)),
-    ("llep E_p > max", lambda L: L.moe_llep_plan(P, 128, 128, 0, P, P, P, P, Z)),
-    ("llep E % E_p", lambda L: L.moe_llep_plan(P, 12, 5, 0, P, P, P, P, Z)),
-    ("llep capacity < 0", lambda L: L.moe_llep_plan(P, 12, 4, -1, P, P, P, P, Z)),
-    ("llep null load", lambda L: L.moe_llep_plan(P, 12, 4, 0, P, P, Z, P, Z)),
-    ("llep dispatch rank", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 4, 4, 10, 64, 12, 2, 5,
-                                                         P, P, P, P, Z)),
-    ("llep dispatch cap", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 4, 0, 10, 64, 12, 2, 21,
-                                                        P, P, P, P, Z)),
-    ("llep dispatch E_p", lambda L: L.moe_llep_dispatch(P, P, P, P, P, P, 5, 0, 10, 64, 12, 2, 5,
-                                                        P, P, P, P, Z)),
-    ("noalloc range", lambda L: L.moe_permute_noalloc(P, P, 10, 64, 8, 2, 4, 8, P, Z, P, P, P, Z)),
-    ("noalloc null offsets", lambda L: L.moe_permute_noalloc(P, P, 10, 64, 8, 2, 0, 8, Z, Z, P, P,
-                                                            P, Z)),
-])
+@pytest.mark.parametrize("case", INVALID, ids=[c[0] for c in INVALID])
 def test_invalid_arguments_rejected_on_host(lib, case):
     name, call = case
     assert call(lib) == -1, name
@@ -148,14 +84,8 @@ def test_invalid_arguments_rejected_on_host(lib, case):
 
 @pytest.mark.skipif(not _no_gpu(), reason="dummy pointers are only safe without a GPU")
 def test_workspace_too_small_rejected(lib):
-    assert lib.moe_permute(P, P, 10, 64, 8, 2, 0, 8, P, Z, P, P, P, P, 16, Z) == -3
-    assert lib.moe_grouped_swiglu_fwd(P, P, 4, 100, 64, 32, P, P, P, P, P, P, P, 16, Z) == -3
-    assert lib.moe_route(P, P, Z, 10, 64, 8, 2, 0, P, P, Z, P, 16, Z) == -3
-    assert lib.moe_route_bwd(P, P, P, P, P, P, 10, 64, 8, 2, 0, P, Z, Z, 1, Z, P, 16, Z) == -3
-    assert lib.moe_ffn_fwd_chunked(P, P, P, 10, 64, 8, 2, 0, 8, 32, P, P, P, 4, P, P, 16, Z,
-                                   Z) == -3
-    assert lib.moe_vocab_loss_fwd(P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
-    assert lib.moe_vocab_loss_bwd(P, P, P, P, P, 10, 64, 100, 16, P, P, P, 16, Z) == -3
+    for call in TOO_SMALL:
+        assert call(lib) == -3
 
 
 @pytest.mark.skipif(not _no_gpu(), reason="dummy pointers are only safe without a GPU")
