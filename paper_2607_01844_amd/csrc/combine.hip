@@ -1,9 +1,12 @@
 // Weighted combination of expert outputs and its backward (gfx950).
 //
 // One wave per token; each lane moves 16 bytes (8 bf16) per row and step, so
-// a wave reads or writes 1 KiB contiguous per instruction.  The k source
-// rows of a token are loaded before they are summed (memory-level
-// parallelism), and the sum runs over the slots in ascending order in fp32.
+// a wave reads or writes 1 KiB contiguous per instruction.  The forward
+// combination reads a token's k source rows one at a time, 8 KiB of a row at
+// once (DRAM-friendly bursts), the next row's loads in flight while the
+// current one is summed; the backward loads all k rows of a 1 KiB column
+// block before it uses them.  Sums run over the slots in ascending order in
+// fp32.
 #include "common.h"
 
 namespace moe {
@@ -43,23 +46,42 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   }
   const int nch = d >> 3;
   uint4* o = reinterpret_cast<uint4*>(out + t * d);
-  for (int c = lane; c < nch; c += 64) {
-    uint4 v[KMAX];
+  // groups of CH chunks per lane (CH KiB of each source row per wave): the
+  // rows are read one at a time, the next row's loads issued before the
+  // current row is summed
+  constexpr int CH = 8;
+  for (int c0 = lane; c0 < nch; c0 += 64 * CH) {
+    float acc[CH][8];
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i)
-      if (i < k && ps[i] >= 0)
-        v[i] = reinterpret_cast<const uint4*>(y + static_cast<int64_t>(ps[i]) * d)[c];
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < CH; ++j)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[j][q] = 0.0f;
+    uint4 cur[CH], nxt[CH];
+    auto load_row = [&](int i, uint4* v) {
+      const uint4* r = reinterpret_cast<const uint4*>(y + static_cast<int64_t>(ps[i]) * d);
+#pragma unroll
+      for (int j = 0; j < CH; ++j)
+        if (c0 + 64 * j < nch) v[j] = r[c0 + 64 * j];
+    };
+    if (0 < k && ps[0] >= 0) load_row(0, cur);
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) {
+      if (i + 1 < KMAX && i + 1 < k && ps[i + 1] >= 0) load_row(i + 1, nxt);
       if (i < k && ps[i] >= 0) {
-        float f[8];
-        unpack8(v[i], f);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] += gs[i] * f[q];
+        for (int j = 0; j < CH; ++j) {
+          float f[8];
+          unpack8(cur[j], f);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[j][q] += gs[i] * f[q];
+        }
       }
+#pragma unroll
+      for (int j = 0; j < CH; ++j) cur[j] = nxt[j];
     }
-    o[c] = pack8(acc);
+#pragma unroll
+    for (int j = 0; j < CH; ++j)
+      if (c0 + 64 * j < nch) o[c0 + 64 * j] = pack8(acc[j]);
   }
 }
 

@@ -70,9 +70,23 @@ __global__ __launch_bounds__(1024) void perm_scan_kernel(const int32_t* __restri
   __shared__ int tot[1024];
   __shared__ int wsum[16];
   const int e = threadIdx.x;
+  // the walks over the nb blocks below load 8 blocks' values before using
+  // them: a dependent load per block would cost one memory round trip each
+  constexpr int U = 8;
   int run = 0;
   if (e < E_loc) {
-    for (int b = 0; b < nb; ++b) {
+    int b = 0;
+    for (; b + U <= nb; b += U) {
+      int c[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) c[u] = blk_loc[static_cast<int64_t>(b + u) * E_loc + e];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        pre[static_cast<int64_t>(b + u) * E_loc + e] = run;
+        run += c[u];
+      }
+    }
+    for (; b < nb; ++b) {
       const int c = blk_loc[static_cast<int64_t>(b) * E_loc + e];
       pre[static_cast<int64_t>(b) * E_loc + e] = run;
       run += c;
@@ -94,12 +108,27 @@ __global__ __launch_bounds__(1024) void perm_scan_kernel(const int32_t* __restri
   tot[e] = excl;
   if (e < E_loc) {
     offsets[e] = excl;
-    for (int b = 0; b < nb; ++b) pre[static_cast<int64_t>(b) * E_loc + e] += excl;
+    int b = 0;
+    for (; b + U <= nb; b += U) {
+      int v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = pre[static_cast<int64_t>(b + u) * E_loc + e];
+#pragma unroll
+      for (int u = 0; u < U; ++u) pre[static_cast<int64_t>(b + u) * E_loc + e] = v[u] + excl;
+    }
+    for (; b < nb; ++b) pre[static_cast<int64_t>(b) * E_loc + e] += excl;
   }
   if (e == E_loc - 1) offsets[E_loc] = excl + run;
   if (counts_global && e < E) {
-    int s = 0;
-    for (int b = 0; b < nb; ++b) s += blk_glob[static_cast<int64_t>(b) * E + e];
+    int s = 0, b = 0;
+    for (; b + U <= nb; b += U) {
+      int v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = blk_glob[static_cast<int64_t>(b + u) * E + e];
+#pragma unroll
+      for (int u = 0; u < U; ++u) s += v[u];
+    }
+    for (; b < nb; ++b) s += blk_glob[static_cast<int64_t>(b) * E + e];
     counts_global[e] = s;
   }
 }
