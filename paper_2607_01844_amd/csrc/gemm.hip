@@ -44,9 +44,10 @@
 //     gets no forward tiles and zero weight gradients.
 //   * XCD-aware order: gfx950 hands consecutive workgroups to its 8 XCDs in
 //     turn, and each XCD has its own L2.  Logical tiles are laid out so each
-//     XCD runs a contiguous range of them, walked in groups of 8 row tiles:
-//     the 32 tiles an XCD runs at a time form an 8 x 4 block of one expert
-//     that shares 8 row slabs and 4 column slabs of the operands in that L2.
+//     XCD runs a contiguous range of them, walked in groups of 4 or 8 row
+//     tiles: the 32 tiles an XCD runs at a time form a 4 x 8 or 8 x 4 block
+//     of one expert that shares its row and column slabs of the operands in
+//     that L2.
 //   * Dense modes run the same loop on plain products (the router's
 //     backward and the blockwise vocabulary loss) with their own epilogues.
 #include "common.h"
@@ -470,8 +471,11 @@ struct Tables {
 // adjacent and the group's column tiles follow one another.  The 32
 // consecutive tiles an XCD runs at a time then form a GM x 32/GM block
 // that shares GM row slabs and 32/GM column slabs of the operands in that
-// XCD's L2 (instead of 32 row slabs and one column slab).
-constexpr int GM = 8;
+// XCD's L2 (instead of 32 row slabs and one column slab).  Measured best:
+// GM = 4 for the row-grouped products (4 row slabs of activations, 8
+// column slabs of an expert's weights), GM = 8 for the weight gradients and
+// the dense products.
+template <int GM>
 __device__ __forceinline__ void tile_pos(int local, int mt, int nt, int& m, int& n) {
   const int per = GM * nt;
   const int grp = local / per;
@@ -543,7 +547,7 @@ struct TileIter {
       const int b = L / per_b, local = L - b * per_b;
       t.e = b;
       int tm, tn;
-      tile_pos(local, g.MT, g.NT, tm, tn);
+      tile_pos<8>(local, g.MT, g.NT, tm, tn);
       t.m0 = tm * BM;
       t.n0 = tn * (DUAL ? BN / 2 : BN);
       t.seg = b * g.kspan;               // first contraction row of the batch
@@ -565,7 +569,7 @@ struct TileIter {
       const int mt_e = tb.mt(lo + 1) - ms0;
       const int local = L - ms0 * g.NT;
       int tm, tn;
-      tile_pos(local, mt_e, g.NT, tm, tn);
+      tile_pos<4>(local, mt_e, g.NT, tm, tn);
       t.m0 = tm * BM;
       t.n0 = tn * (DUAL ? BN / 2 : BN);
       t.seg = tb.off(lo);
@@ -591,7 +595,7 @@ struct TileIter {
       t.e = __builtin_amdgcn_readfirstlane(e);
       const int local = L - unit * tb.nz(e);
       int tm, tn;
-      tile_pos(local, g.MT, g.NT, tm, tn);
+      tile_pos<8>(local, g.MT, g.NT, tm, tn);
       t.m0 = tm * BM;
       t.n0 = tn * (DUAL ? BN / 2 : BN);
       t.seg = tb.off(e);
