@@ -1152,9 +1152,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       auto load_frags = [&](Frags& F, int sa, int sb, int sub) __attribute__((always_inline)) {
         const lds_char* ta = ring + sa * UNIT + (sub >> 1) * HALF;
         const lds_char* tbl = ring + (NA + sb) * UNIT + (sub >> 1) * HALF;
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < 4; ++i) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
-  #pragma unroll
+#pragma unroll
         for (int jj = 0; jj < 2; ++jj) F.b[jj] = BOp::frag(tbl, brow[jj], sub & 1, lane);
       };
       // the 8 MFMAs of one sub-step, kept in this order and apart from any
@@ -1393,12 +1393,12 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     auto load_frags = [&](Frags& F, int sa, int sb, int sub) __attribute__((always_inline)) {
       const lds_char* ta = ring + sa * UNIT + (A_N ? (sub >> 1) * HALF : 0);
       const lds_char* tb = ring + (NA + sb) * UNIT + (B_N ? (sub >> 1) * HALF : 0);
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < 4; ++i) {
         if constexpr (A_N) F.a[i] = AOp::frag(ta, arow[i], sub & 1, lane);
         else F.a[i] = AOp::frag(ta, arow[i] + l32, sub, lh);
       }
-  #pragma unroll
+#pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
         if constexpr (B_K) F.b[jj] = BOp::frag(tb, brow[jj] + l32, sub, lh);
         else F.b[jj] = BOp::frag(tb, brow[jj], sub & 1, lane);
@@ -1418,9 +1418,9 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       }
     };
     auto mma = [&](const Frags& F) __attribute__((always_inline)) {
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < 4; ++i)
-  #pragma unroll
+#pragma unroll
         for (int jj = 0; jj < 2; ++jj)
           acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.b[jj], F.a[i], acc[i][jj], 0, 0, 0);
     };
