@@ -27,8 +27,9 @@
 //     both operands with transposing LDS reads, run the same ring in a
 //     ping-pong schedule when their tiles are long: the two waves of each
 //     SIMD take turns, one running a half step of MFMAs while the other
-//     issues loads and reads its next fragments, with a barrier between
-//     turns.
+//     reads its next fragments, with a barrier between turns.  One group of
+//     four waves issues all operand loads and the other all output stores,
+//     so no wave that waits for operands has stores ahead of them.
 //   * Operands stored K-contiguous (activations in the forward pass and the
 //     data gradients, weights in the data gradients) sit in LDS as
 //     [256 rows][64 k] and feed the MFMA with ds_read_b128.  Operands stored
@@ -1120,15 +1121,14 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
   };
 
   const Tables tb{g.mt_start, g.offsets, g.wk_start, g.nz_start};
-  // The weight gradients (grouped, and the vocabulary's dW) store both
-  // operands with the output index contiguous and read every fragment with
-  // two transposing LDS reads.  When their tiles are long (at least 16 K
-  // steps on average) they run the ping-pong schedule below, which keeps
-  // those reads out of the MFMA stream; its tile change costs an extra
-  // phase, so short tiles, the router's dW (short token chunks) and every
-  // other mode run the single-barrier schedule after it.  The choice is
-  // uniform over the launch.
-  constexpr bool PP_OK = A_N && !B_K && MODE != RT_DW;
+  // Schedule choice (uniform over the launch).  The weight gradients
+  // (grouped, and the vocabulary's dW) read both operands with transposing
+  // LDS reads; when their tiles are long (at least 16 K steps on average)
+  // they run the ping-pong schedule below, which keeps those reads out of
+  // the MFMA stream.  Its tile change costs five extra phases, so short
+  // tiles, the router's dW (short token chunks) and every other mode run the
+  // single-barrier schedule after it.
+  constexpr bool PP_OK = WGRAD || MODE == VOC_DW;
   bool use_pp = false;
   if constexpr (PP_OK) {
     if constexpr (DENSE) use_pp = g.kspan >= 16 * BK;
@@ -1138,10 +1138,11 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
     if constexpr (PP_OK) {
       // ---------------------------------------------------------- LDS ring
       // NA = 2 slots of UNIT bytes for operand A (loaded one step ahead), then
-      // 3 for operand B (two steps ahead).
+      // 3 for operand B (two steps ahead).  Both operands are N-contiguous.
       constexpr int NA = 2;
       using St = NStream<4>;
-      static_assert(NRING - NA == 3 && 2 * St::LH == 8, "the wait counts below assume this ring");
+      static_assert(A_N && !B_K && NRING - NA == 3 && 2 * St::LH == 8,
+                    "the wait counts below assume this ring and 8 loads per wave and step");
       lds_char* const ring = (lds_char*)(lds);  // address-space cast
       const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
       struct Frags {
@@ -1176,30 +1177,118 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         __builtin_amdgcn_sched_barrier(0);
       };
 
+      // ------------------------------------------------------ write-out
+      // A finished tile leaves in four passes, one per 32-row block i of
+      // every wave's 128 x 64 accumulator block: each wave writes its block i
+      // as bf16 into its 4 KiB patch of a pass slot (wave X at X * 4 KiB),
+      // and after the barrier each wave of group 1 reads two patches (of wave
+      // q of group 0 and its own) and stores them.  The patch layouts carry
+      // XOR swizzles that keep the 64 banks conflict-free (bf16 rows 16..31
+      // hold their two 8-byte halves swapped).
+      typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+      typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+      auto unswap = [](uint4 v, int r) __attribute__((always_inline)) {
+        return (r & 16) ? make_uint4(v.z, v.w, v.x, v.y) : v;
+      };
+      auto put_block = [&](auto IC, lds_char* patch) __attribute__((always_inline)) {
+        constexpr int i = IC;
+        const int ln = opaque(threadIdx.x & 63);
+        const int p32 = ln & 31, ph = ln >> 5;
+        auto put8 = [&](int off, uint2 v) __attribute__((always_inline)) {
+          *(__attribute__((address_space(3))) u32x2v*)(patch + off) = u32x2v{v.x, v.y};
+        };
+        if constexpr (DUAL) {
+          // gate [32][32] bf16 at +0, up at +2048; 64-byte rows, 16-byte
+          // chunk c of row r at c ^ ((r / 4) % 4)
+          static_for<4>([&](auto Q) {
+            constexpr int q = Q;
+            const int off = p32 * 64 + ((q ^ ((p32 >> 2) & 3)) << 4) + ((ph ^ (p32 >> 4)) & 1) * 8;
+            put8(off, pack4(acc[i][0][4 * q], acc[i][0][4 * q + 1], acc[i][0][4 * q + 2], acc[i][0][4 * q + 3]));
+            put8(2048 + off, pack4(acc[i][1][4 * q], acc[i][1][4 * q + 1], acc[i][1][4 * q + 2],
+                                   acc[i][1][4 * q + 3]));
+          });
+        } else {
+          // [32][64] bf16, 128-byte rows, 16-byte chunk c of row r at
+          // c ^ ((r / 2) % 8)
+          static_for<2>([&](auto J) {
+            static_for<4>([&](auto Q) {
+              constexpr int j = J, q = Q;
+              const int off = p32 * 128 + (((4 * j + q) ^ ((p32 >> 1) & 7)) << 4) + ((ph ^ (p32 >> 4)) & 1) * 8;
+              put8(off, pack4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
+            });
+          });
+        }
+      };
+      // block i of wave X's accumulators (tile tl), from its patch to memory
+      auto store_block = [&](const Tile& tl, auto IC, const lds_char* patch, int X) __attribute__((always_inline)) {
+        constexpr int i = IC;
+        const int e = tl.e, m0 = tl.m0, n0 = tl.n0;
+        const int ln = opaque(threadIdx.x & 63);
+        const int mvalid = DENSE ? (g.dM - m0) : ((MODE == WGRAD_GATE_UP ? d : f) - m0);
+        const int rb = (X & 1) * 128 + 32 * i;  // tile row of the block's first row
+        const int xn = X >> 1;                  // the producing wave's column group
+        if (rb >= mvalid) return;
+        auto get16 = [&](int off) __attribute__((always_inline)) {
+          const u32x4v v = *(const __attribute__((address_space(3))) u32x4v*)(patch + off);
+          return make_uint4(v[0], v[1], v[2], v[3]);
+        };
+        if constexpr (DUAL) {
+          static_for<2>([&](auto Tt) {
+            constexpr int t = Tt;
+            const int r = 16 * t + (ln >> 2), c = ln & 3;
+            const int off = r * 64 + ((c ^ ((r >> 2) & 3)) << 4);
+            const uint4 hgv = unswap(get16(off), r), huv = unswap(get16(2048 + off), r);
+            const int rt = rb + r, col = n0 + xn * 32 + 8 * c;
+            if (rt < mvalid && col < f) {
+              const int64_t o = e * wdf + (int64_t)(m0 + rt) * f + col;
+              *reinterpret_cast<uint4*>(g.dwg + o) = hgv;
+              *reinterpret_cast<uint4*>(g.dwu + o) = huv;
+            }
+          });
+        } else {
+          static_for<4>([&](auto Tt) {
+            constexpr int t = Tt;
+            const int r = 8 * t + (ln >> 3), c = ln & 7;
+            const uint4 v = unswap(get16(r * 128 + ((c ^ ((r >> 1) & 7)) << 4)), r);
+            const int rt = rb + r, col = n0 + xn * 64 + 8 * c;
+            if (rt < mvalid && col < (DENSE ? g.dN : d)) {
+              uint16_t* out;
+              if constexpr (MODE == WGRAD_DOWN) out = g.dwd + e * wdf + (int64_t)(m0 + rt) * d;
+              else out = static_cast<uint16_t*>(g.dc) + (int64_t)(m0 + rt) * g.c_ld + g.cc0;  // VOC_DW
+              *reinterpret_cast<uint4*>(out + col) = v;
+            }
+          });
+        }
+      };
+
       // -------------------------------------------------------- tile stream
       // Waves 0-3 (group 0, one per SIMD) and waves 4-7 (group 1) each hold
       // half of the tile's B-side columns.  Time runs in phases separated by
-      // workgroup barriers.  In a memory phase a group issues its operand
-      // loads and reads the fragments of one half step (two sub-steps) from
-      // LDS; in the compute phase that follows it runs that half step's 16
-      // MFMAs per wave and nothing else.  Group 1 runs one phase behind group
-      // 0, so on every SIMD one wave issues MFMAs while the other moves data.
-      // Every wave passes the same number of barriers: two per half step, one
-      // between consecutive tiles, and one more at the start (group 1: the
-      // stagger) or at the end (group 0: its wait before the last epilogue).
-      //   Group 0 loads all of operand A (each wave a quarter of a step), step
-      // j + 1 at the start of step j into the slot step j - 1 freed; its wait
-      // for it closes step j.  Group 1 loads all of operand B, step j + 2 at
-      // the start of step j; its wait for step j + 1 closes its second memory
-      // phase of step j.
-      //   Loads for steps past the current tile fetch the next tile's first
-      // steps (its streams are prepared before the tile's last two steps).  A
-      // B step that would lie beyond the next tile (after a tile of one step)
-      // is issued when its tile becomes the next one, before it is needed.
-      // Between tiles both groups write out the finished tile in one phase
-      // (one more barrier for each); the output patches sit in B's slot of that
-      // tile's last step, so its refill (step 2 of the new tile) waits for
-      // group 1's second memory phase of the new tile.
+      // workgroup barriers: in a memory phase a group reads the fragments of
+      // one half step (two sub-steps) from LDS, in the compute phase that
+      // follows it runs that half step's 16 MFMAs per wave and nothing else;
+      // group 1 runs one phase behind group 0, so on every SIMD one wave
+      // issues MFMAs while the other moves data.
+      //   The roles are split: group 0 issues every operand load and never
+      // stores, group 1 issues every output store and never waits for vector
+      // memory.  A wave's vector-memory counter completes in issue order, so
+      // a wave that stored a tile and then waits for the next tile's operands
+      // would wait for its stores too.  Group 0 loads A step j + 1 in its
+      // first memory phase of step j and B up to step j + 2 in its second
+      // (a B step that lay beyond the next tile when its turn came, after a
+      // tile of one step, goes out here too), and waits for A and B step
+      // j + 1 at the end of step j.  Loads for steps past the current tile
+      // fetch the next tile's first steps (its streams are prepared before
+      // the tile's last two steps).
+      //   Between tiles, group 0 first waits out group 1's last half step;
+      // then four write-out passes run in the two slots the finished tile's
+      // last step used (A's and B's), group 1 storing pass p - 1 while every
+      // wave writes pass p.  Group 0's first memory phase of the new tile
+      // runs beside group 1's store of the last pass; A step 1 and B step 2
+      // of the new tile go to those two slots after it.  Every wave passes
+      // the same number of barriers: two per half step, five per tile
+      // change, and one more at the start (group 1: the stagger) or at a
+      // tile change with no tile after it (group 0).
       const int grp = w >> 2, wq = w & 3;
       auto run = [&](auto GC) __attribute__((always_inline)) {
         constexpr int G = GC;
@@ -1207,38 +1296,28 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         it.init(g, tb);
         Tile tc = it.next(g, tb);
         if (!tc.valid) return;
-        St cur, nxt;  // this group's loads of the current and of the next tile
-        auto prep = [&](const Tile& t, St& st) __attribute__((always_inline)) {
-          if constexpr (G == 0) {
-            AOp o;
-            setupA(t, o);
-            st.setup(o, wq, lane);
-          } else {
-            BOp o;
-            setupB(t, o);
-            st.setup(o, wq, lane);
-          }
+        St ca, cb, na, nb;  // group 0: A and B loads of the current and of the next tile
+        auto prep = [&](const Tile& t, St& sa, St& sb) __attribute__((always_inline)) {
+          AOp oa;
+          setupA(t, oa);
+          sa.setup(oa, wq, lane);
+          BOp ob;
+          setupB(t, ob);
+          sb.setup(ob, wq, lane);
         };
-        // all of one step's loads of this group's operand into its ring slot
-        auto issue = [&](const St& st, int j, int slot) __attribute__((always_inline)) {
-          const uint32_t u = lds0 + (G == 0 ? slot : NA + slot) * UNIT;
+        // one step of one operand into LDS unit `u` (its two halves)
+        auto issue = [&](const St& st, int j, uint32_t u) __attribute__((always_inline)) {
           st.issue(j, 0, u, wq);
           st.issue(j, 1, u + HALF, wq);
         };
         zero_acc();
-        prep(tc, cur);
         int ra = 0, rb = 0;  // ring slots (A: 0..1, B: 0..2) of the current step
-        int bl = 0;          // group 1: first B step, counted in the current tile, not yet issued
-        // prologue: A step 0 (group 0), B steps 0 and 1 (group 1)
+        int bl = 0;          // group 0: first B step, counted in the current tile, not yet issued
         if constexpr (G == 0) {
-          issue(cur, 0, 0);
-        } else {
-          issue(cur, 0, 0);
-          bl = 1;
-          if (tc.nk > 1) {
-            issue(cur, 1, 1);
-            bl = 2;
-          }
+          // prologue: A step 0, B steps 0 and 1 (of this tile)
+          prep(tc, ca, cb);
+          issue(ca, 0, lds0);
+          for (bl = 0; bl < 2 && bl < tc.nk; ++bl) issue(cb, bl, lds0 + (NA + bl) * UNIT);
         }
         wait_vmcnt<0>();
         phase_end();
@@ -1249,31 +1328,41 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         bool has_prev = false;
         while (true) {
           if (has_prev) {
-            // The previous tile's outputs, through patches in B's slot of its
-            // last step, both groups in one phase: group 0 first waits out
-            // group 1's last half step, and group 1 starts its first memory
-            // phase of the new tile one phase later (group 0's runs beside the
-            // epilogues).
+            // write-out passes in the finished tile's last-step slots
+            lds_char* const S0 = ring + (ra ^ 1) * UNIT;
+            lds_char* const S1 = ring + (NA + (rb == 0 ? 2 : rb - 1)) * UNIT;
             if constexpr (G == 0) phase_end();
             lgkm_drained();
-            epilogue(tp, ring + (NA + (rb == 0 ? 2 : rb - 1)) * UNIT + w * PATCH_BYTES);
+            static_for<4>([&](auto P) {
+              constexpr int p = P;
+              put_block(P, (p & 1 ? S1 : S0) + w * PATCH_BYTES);
+              if constexpr (G == 1 && p > 0) {
+                lds_char* const Sp = (p - 1) & 1 ? S1 : S0;
+                store_block(tp, std::integral_constant<int, p - 1>{}, Sp + wq * PATCH_BYTES, wq);
+                store_block(tp, std::integral_constant<int, p - 1>{}, Sp + w * PATCH_BYTES, w);
+              }
+              phase_end();
+            });
             zero_acc();
             if constexpr (G == 1) {
+              store_block(tp, std::integral_constant<int, 3>{}, S1 + wq * PATCH_BYTES, wq);
+              store_block(tp, std::integral_constant<int, 3>{}, S1 + w * PATCH_BYTES, w);
               if (tc.valid) phase_end();
             }
           }
           if (!tc.valid) break;
           const int nk = tc.nk;
-          int nkn = 0;  // steps of the next tile (0: none)
-          // step j counted in the current tile (past nk: the next tile's) into
-          // `slot`, if its tile is the current or the next one
-          auto issue_at = [&](int j, int slot) __attribute__((always_inline)) {
+          int nkn = 0;  // group 0: steps of the next tile (0: none)
+          // step j counted in the current tile (past nk: the next tile's) of
+          // operand A or B into LDS unit `u`; false if its tile is neither
+          // the current nor the next one
+          auto issue_at = [&](bool b_side, int j, uint32_t u) __attribute__((always_inline)) {
             if (j < nk) {
-              issue(cur, j, slot);
+              issue(b_side ? cb : ca, j, u);
               return true;
             }
             if (j - nk < nkn) {
-              issue(nxt, j - nk, slot);
+              issue(b_side ? nb : na, j - nk, u);
               return true;
             }
             return false;
@@ -1282,26 +1371,11 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
           // TAIL: its loads may reach past the tile (the next one or nothing).
           auto step = [&](int s, auto TAILC) __attribute__((always_inline)) {
             constexpr bool TAIL = TAILC;
-            bool b8 = false;  // group 1: this step issued B step s + 2 (the last of its loads)
-            // ---- memory phase, first half
+            // ---- memory phase, first half (group 0: A step s + 1)
             if constexpr (G == 0) {
-              if constexpr (TAIL) issue_at(s + 1, ra ^ 1);
-              else issue(cur, s + 1, ra ^ 1);
-            } else {
-              // B up to step s + 2; at a tile's first step only up to step 1
-              // (step 2 goes to the slot that held the output patches)
-              const int tgt = s == 0 ? 1 : s + 2;
-              while (bl <= tgt) {
-                const int d3 = rb + bl - s;  // 0 .. 4
-                const int slot = d3 >= 3 ? d3 - 3 : d3;
-                if constexpr (TAIL) {
-                  if (!issue_at(bl, slot)) break;
-                } else {
-                  issue(cur, bl, slot);
-                }
-                ++bl;
-              }
-              b8 = s != 0 && bl == s + 3;
+              const uint32_t u = lds0 + (ra ^ 1) * UNIT;
+              if constexpr (TAIL) issue_at(false, s + 1, u);
+              else issue(ca, s + 1, u);
             }
             lgkm_drained();
             load_frags(F0, ra, rb, 0);
@@ -1311,28 +1385,32 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
             mma(F0);
             mma(F1);
             phase_end();
-            // ---- memory phase, second half
-            if constexpr (G == 1) {
-              if (s == 0 && bl == 2) {
-                if (issue_at(2, rb == 0 ? 2 : rb - 1)) {
-                  bl = 3;
-                  b8 = true;
+            // ---- memory phase, second half (group 0: B up to step s + 2)
+            bool b8 = false;  // group 0: B step s + 2 went out this step, the last of its loads
+            if constexpr (G == 0) {
+              while (bl <= s + 2) {
+                const int d3 = rb + bl - s;  // 1 or 2: B steps s and earlier are in place
+                const uint32_t u = lds0 + (NA + (d3 >= 3 ? d3 - 3 : d3)) * UNIT;
+                if constexpr (TAIL) {
+                  if (!issue_at(true, bl, u)) break;
+                } else {
+                  issue(cb, bl, u);
                 }
+                ++bl;
               }
+              b8 = bl == s + 3;
             }
             load_frags(F0, ra, rb, 2);
             load_frags(F1, ra, rb, 3);
-            if constexpr (G == 1) {
-              // B step s + 1 has landed (step s + 2, issued after it, may still
-              // be in flight)
+            phase_end();
+            // ---- compute phase, second half; group 0 then waits for A and B
+            // step s + 1 (B step s + 2, issued after them, may still fly)
+            mma(F0);
+            mma(F1);
+            if constexpr (G == 0) {
               if (b8) wait_vmcnt<8>();
               else wait_vmcnt<0>();
             }
-            phase_end();
-            // ---- compute phase, second half
-            mma(F0);
-            mma(F1);
-            if constexpr (G == 0) wait_vmcnt<0>();  // A step s + 1 has landed
             phase_end();
             ra ^= 1;
             rb = rb == 2 ? 0 : rb + 1;
@@ -1341,16 +1419,21 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
           for (; s + 2 < nk; ++s) step(s, std::false_type{});
           // the last two steps load into the next tile: prepare its streams
           const Tile tn = it.next(g, tb);
-          if (tn.valid) {
-            prep(tn, nxt);
-            nkn = tn.nk;
+          if constexpr (G == 0) {
+            if (tn.valid) {
+              prep(tn, na, nb);
+              nkn = tn.nk;
+            }
           }
           for (; s < nk; ++s) step(s, std::true_type{});
           tp = tc;
           has_prev = true;
           tc = tn;
-          cur = nxt;
-          if constexpr (G == 1) bl -= nk;
+          if constexpr (G == 0) {
+            ca = na;
+            cb = nb;
+            bl -= nk;
+          }
         }
         wait_vmcnt<0>();
       };
