@@ -255,13 +255,15 @@ def vendor_batched(wl, steps: int):
     return out
 
 
-def llep_leg(steps: int, E_p: int = 8, name: str = "large_skew"):
+def llep_leg(steps: int, E_p: int = 8, name: str = "large_skew", granule: int = 256):
     """Least-loaded expert parallelism on one GPU's view of E_p ranks
     (Sec. 3.3): the skewed workload's real routing, the plan, and the
     forward expert GEMMs of every rank under standard expert parallelism
     (each rank its own E/E_p experts) and under the plan.  The slowest rank
     sets the layer's pace on E_p GPUs; the plan and the dispatch are timed
-    too."""
+    too.  The plan counts load in units of `granule` rows (the grouped
+    GEMM's row tile: a rank's GEMM time follows its tile count); the plan
+    that balances rows (granule 1) is reported beside it."""
     from paper_2607_01844_amd import moe as m
     wl = W.WORKLOADS[name]
     inp = W.make_inputs(wl, seed=0, device="cuda", with_grad=False)
@@ -280,33 +282,59 @@ def llep_leg(steps: int, E_p: int = 8, name: str = "large_skew"):
         torch.cuda.synchronize()
         return start.elapsed_time(stop) / n
 
-    plan = {}
-    plan_ms = timed(lambda: plan.update(zip(("lo", "hi", "load", "ns"),
-                                            m.moe_llep_plan(pm["counts_global"], E_p))))
+    plans, plan_ms = {}, {}
+    for g in (granule, 1):
+        box = {}
+        plan_ms[g] = timed(lambda: box.update(zip(("lo", "hi", "load", "ns"),
+                                                  m.moe_llep_plan(pm["counts_global"], E_p, 0, g))))
+        plans[g] = box
     counts = pm["counts_global"].cpu().numpy()
     ep_load = counts.reshape(E_p, G).sum(axis=1)
-    cap_ep, cap_ll = int(ep_load.max()), -(-wl.T * wl.k // E_p)
+    cap_ep = int(ep_load.max())
     w = (inp["w_gate"], inp["w_up"], inp["w_down"])
-    ep_ms, ll_ms, disp_ms = [], [], []
+
+    def tiles(rows):
+        return int(sum(-(-int(n) // 256) for n in rows))
+
+    ep_ms, ep_tiles = [], []
+    ll_ms, ll_tiles, disp_ms = {g: [] for g in plans}, {g: [] for g in plans}, []
     for r in range(E_p):
         sl = slice(r * G, (r + 1) * G)
         pr = m.moe_permute(inp["x"], idx, E, r * G, G, cap=cap_ep)
         ws = tuple(t[sl] for t in w)
         ep_ms.append(timed(lambda: m.moe_grouped_swiglu_fwd(pr["x_perm"], pr["expert_offsets"],
                                                             *ws, cap=cap_ep)))
-        box = {}
-        disp_ms.append(timed(lambda: box.update(m.moe_llep_dispatch(
-            inp["x"], idx, pm["expert_offsets"], pm["dst"], plan["lo"], plan["hi"], r, cap_ll))))
-        ll_ms.append(timed(lambda: m.moe_grouped_swiglu_fwd(box["x_perm"], box["expert_offsets"],
-                                                            *w, cap=cap_ll)))
-    load = plan["load"].cpu().numpy()
+        ep_tiles.append(tiles(counts[sl]))
+        for g, plan in plans.items():
+            cap_ll = max(int(plan["load"].max().item()), 1)
+            box = {}
+            dm = timed(lambda: box.update(m.moe_llep_dispatch(
+                inp["x"], idx, pm["expert_offsets"], pm["dst"], plan["lo"], plan["hi"], r, cap_ll)))
+            if g == granule:
+                disp_ms.append(dm)
+            ll_ms[g].append(timed(lambda: m.moe_grouped_swiglu_fwd(box["x_perm"], box["expert_offsets"],
+                                                                   *w, cap=cap_ll)))
+            ll_tiles[g].append(tiles((plan["hi"][r] - plan["lo"][r]).cpu().numpy()))
+
+    def leg(g):
+        return {"rank_rows": plans[g]["load"].cpu().numpy().tolist(),
+                "rank_row_tiles": ll_tiles[g],
+                "weight_shipments": int(plans[g]["ns"].item()),
+                "slowest_rank_fwd_gemm_ms": round(max(ll_ms[g]), 4),
+                "straggler_speedup": round(max(ep_ms) / max(ll_ms[g]), 3),
+                "plan_ms": round(plan_ms[g], 4)}
+
+    main = leg(granule)
     return {"workload": f"{name} routing, E_p={E_p} ranks of {G} experts",
-            "standard_ep_rank_rows": ep_load.tolist(), "llep_rank_rows": load.tolist(),
-            "weight_shipments": int(plan["ns"].item()),
+            "granule_rows": granule,
+            "standard_ep_rank_rows": ep_load.tolist(), "standard_ep_rank_row_tiles": ep_tiles,
+            "llep_rank_rows": main["rank_rows"], "llep_rank_row_tiles": main["rank_row_tiles"],
+            "weight_shipments": main["weight_shipments"],
             "standard_ep_slowest_rank_fwd_gemm_ms": round(max(ep_ms), 4),
-            "llep_slowest_rank_fwd_gemm_ms": round(max(ll_ms), 4),
-            "straggler_speedup": round(max(ep_ms) / max(ll_ms), 3),
-            "plan_ms": round(plan_ms, 4), "dispatch_ms_per_rank": round(float(np.mean(disp_ms)), 4)}
+            "llep_slowest_rank_fwd_gemm_ms": main["slowest_rank_fwd_gemm_ms"],
+            "straggler_speedup": main["straggler_speedup"],
+            "plan_ms": main["plan_ms"], "dispatch_ms_per_rank": round(float(np.mean(disp_ms)), 4),
+            "row_balanced_plan": leg(1)}
 
 
 def vocab_loss(steps: int, warmup: int):

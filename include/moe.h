@@ -54,6 +54,7 @@ extern "C" {
 #define MOE_MAX_E 1024
 #define MOE_MAX_DIM 262144
 #define MOE_LLEP_MAX_RANKS 64
+#define MOE_LLEP_MAX_GRANULE 65536
 #define MOE_PERMUTE_NOALLOC_MAX_BYTES 8388608
 
 typedef uint16_t moe_bf16;
@@ -316,25 +317,34 @@ int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* 
  * products, together with the weights of those experts, to a rank below
  * it, which then computes them; the set of products does not change.  The
  * paper does not give the planning steps; this library's plan is:
+ *   - load is counted in units of `granule` = g rows: g = 1 counts rows;
+ *     g = the grouped GEMM's row-tile height (256) counts the tiles a
+ *     rank's expert products run, since a window of w rows costs
+ *     ceil(w / g) tiles however small w is;
  *   - E experts on E_p ranks, expert e at home on rank e / (E / E_p);
- *     L = sum of counts; capacity C = max(capacity, ceil(L / E_p));
+ *     u_e = ceil(counts[e] / g), U = sum u_e; capacity
+ *     C = max(ceil(capacity / g), ceil(U / E_p)) units;
  *   - every rank keeps its own experts, ascending, while its load stays
- *     <= C; the rest of an expert is its spill;
- *   - experts with spill, largest spill first (ties: lower index), hand it
- *     out in pieces, each to the currently least loaded rank (ties: lower
- *     rank) and as large as that rank's room below C.
+ *     <= C units; the rest of an expert is its spill;
+ *   - experts with spill, largest spill (in units) first (ties: lower
+ *     index), hand it out in pieces of whole units, each to the rank with
+ *     the fewest units (ties: lower rank) and as large as that rank's room
+ *     below C; a piece of t units is t * g rows or what is left.
  * Expert e's assignments in the layer's row order (ascending t*k + i, the
  * order of moe_permute) are cut into consecutive windows: the home rank's
- * [0, keep) first, then the pieces in the order handed out.  Every rank's
- * load is <= C; a piece on a rank other than the home is one shipment of
- * that expert's weights.
+ * [0, keep) first, then the pieces in the order handed out.  Every window
+ * but an expert's last is a whole number of units (no window splits a
+ * tile); every rank's load is <= C units, so its largest tile count is the
+ * least any plan can reach, ceil(U / E_p), when capacity = 0; a piece on a
+ * rank other than the home is one shipment of that expert's weights.
  *
  * moe_llep_plan: counts [E] int32 (assignments per expert over all tokens,
  * e.g. moe_permute's counts_global) -> win_lo, win_hi [E_p][E] int32 (rank
  * r computes rows [win_lo[r][e], win_hi[r][e]) of expert e; empty windows
- * are [0, 0)), load [E_p] int32, n_ship [1] int32.  One workgroup, all on
- * the device (no host round trip for the counts).  Limits: 1 <= E_p <=
- * MOE_LLEP_MAX_RANKS, E a multiple of E_p, capacity >= 0.
+ * are [0, 0)), load [E_p] int32 (each rank's rows, at most C * g),
+ * n_ship [1] int32.  One workgroup, all on the device (no host round trip
+ * for the counts).  Limits: 1 <= E_p <= MOE_LLEP_MAX_RANKS, E a multiple
+ * of E_p, capacity >= 0, 1 <= granule <= MOE_LLEP_MAX_GRANULE.
  *
  * moe_llep_dispatch: one rank's share of the layer under a plan.  Inputs:
  * x [T][d], topk_idx [T][k], and the permutation of ALL experts from
@@ -343,16 +353,16 @@ int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const int32_t* 
  * the moe_permute layout over all E experts: offsets_r [E + 1] (expert e's
  * rows at [offsets_r[e], offsets_r[e + 1]), clamped to cap), row_src_r
  * [cap], dst_r [T*k] (-1 for assignments other ranks compute) and x_perm_r
- * [cap][d].  cap must be >= the rank's load, which the plan bounds by
- * max(capacity, ceil(T*k / E_p)); rows past cap are dropped.  The rank then
+ * [cap][d].  cap must be >= the rank's load (the plan's load output: at
+ * most C * g rows, and never more than T*k); rows past cap are dropped.  The rank then
  * runs moe_grouped_swiglu_fwd/_bwd with num_local = E on these buffers (a
  * shipped expert's weights are read from the [E] weight arrays) and
  * moe_combine into its partial output; the partial outputs of all ranks
  * sum to the layer's output, and every y_perm row equals the one the whole
  * layer computes for that assignment.
  */
-int moe_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* win_lo,
-                  int32_t* win_hi, int32_t* load, int32_t* n_ship, void* stream);
+int moe_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int granule,
+                  int32_t* win_lo, int32_t* win_hi, int32_t* load, int32_t* n_ship, void* stream);
 int moe_llep_dispatch(const moe_bf16* x, const int32_t* topk_idx, const int32_t* offsets_all,
                       const int32_t* dst_all, const int32_t* win_lo, const int32_t* win_hi,
                       int E_p, int rank, int64_t T, int d, int E, int k, int64_t cap,

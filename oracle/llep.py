@@ -13,58 +13,73 @@ the LLEP paper, which is not available), so the plan below is a reading of
 that description, fully specified so that the device planner can be checked
 bit for bit:
 
+  * Load is counted in units of g rows (the granule; g = 1 counts rows, g =
+    the grouped GEMM's row-tile height counts the tiles a rank's products
+    run, since a window of w rows costs ceil(w / g) tiles whatever w is).
   * E experts on E_p ranks, expert e at home on rank e // (E / E_p);
-    n_e = assignments of expert e (over all tokens); L = sum n_e;
-    capacity C = max(capacity_in, ceil(L / E_p)).
+    n_e = assignments of expert e (over all tokens), u_e = ceil(n_e / g) its
+    units, U = sum u_e; capacity C = max(ceil(capacity_in / g),
+    ceil(U / E_p)) units.
   * Keep at home: every rank walks its experts in ascending index and keeps
-    min(n_e, C - load) of each; the rest of expert e is its spill s_e.
+    min(u_e, C - load) units of each (its first min(n_e, that * g) rows);
+    the rest of expert e, in units, is its spill s_e.
   * Move to the least loaded: experts with s_e > 0, in order of decreasing
     s_e (ties: lower index first), hand their spill in pieces to the rank
-    with the smallest load (ties: lower rank), each piece as large as that
-    rank's room C - load allows, until nothing is left.
+    with the smallest load in units (ties: lower rank), each piece as many
+    units as that rank's room C - load allows, until nothing is left; a
+    piece of t units is t * g rows, or what is left of the expert.
   * Expert e's assignments, in the layer's stable row order (ascending
     assignment index t*k + i), are cut into consecutive windows: the home
     rank's [0, keep_e) first, then the pieces in the order they were handed
     out.  Every piece on a rank other than the home is one weight shipment.
+    Every window but an expert's last starts and ends on a multiple of g,
+    so no window splits a unit and a rank's unit load is the sum of
+    ceil(window / g) over its windows.
 """
 from __future__ import annotations
 
 import numpy as np
 
 
-def llep_plan(counts, E_p: int, capacity: int = 0):
+def llep_plan(counts, E_p: int, capacity: int = 0, granule: int = 1):
     """Returns (lo [E_p, E], hi [E_p, E], load [E_p], n_ship) as int64 numpy
-    arrays / int.  Rank r computes rows [lo[r, e], hi[r, e]) of expert e."""
+    arrays / int.  Rank r computes rows [lo[r, e], hi[r, e]) of expert e;
+    load is each rank's rows (its units are at most the capacity C)."""
     n = [int(c) for c in counts]
     E = len(n)
-    assert E_p >= 1 and E % E_p == 0
+    g = int(granule)
+    assert E_p >= 1 and E % E_p == 0 and g >= 1
     G = E // E_p
-    total = sum(n)
-    C = max(int(capacity), -(-total // E_p))
+    u = [-(-c // g) for c in n]
+    C = max(-(-int(capacity) // g), -(-sum(u) // E_p))
     lo = np.zeros((E_p, E), np.int64)
     hi = np.zeros((E_p, E), np.int64)
-    load = [0] * E_p
-    spill = [0] * E
+    load_u = [0] * E_p
+    load_rows = [0] * E_p
+    spill = [0] * E  # units
     for r in range(E_p):
         for e in range(r * G, (r + 1) * G):
-            keep = min(n[e], C - load[r])
-            hi[r, e] = keep
-            load[r] += keep
-            spill[e] = n[e] - keep
+            keep = min(u[e], C - load_u[r])
+            hi[r, e] = min(n[e], keep * g)
+            load_u[r] += keep
+            load_rows[r] += int(hi[r, e])
+            spill[e] = u[e] - keep
     order = sorted((e for e in range(E) if spill[e] > 0), key=lambda e: (-spill[e], e))
     n_ship = 0
     for e in order:
-        start = n[e] - spill[e]
+        start = (u[e] - spill[e]) * g  # rows kept at home
         while spill[e] > 0:
-            r = min(range(E_p), key=lambda q: (load[q], q))
-            take = min(spill[e], C - load[r])
+            r = min(range(E_p), key=lambda q: (load_u[q], q))
+            take = min(spill[e], C - load_u[r])
             assert take > 0, "capacity below the total"
-            lo[r, e], hi[r, e] = start, start + take
-            load[r] += take
-            start += take
+            rows = min(n[e] - start, take * g)
+            lo[r, e], hi[r, e] = start, start + rows
+            load_u[r] += take
+            load_rows[r] += rows
+            start += rows
             spill[e] -= take
             n_ship += 1
-    return lo, hi, np.array(load, np.int64), n_ship
+    return lo, hi, np.array(load_rows, np.int64), n_ship
 
 
 def rank_rows(topk_idx, lo, hi, r: int):

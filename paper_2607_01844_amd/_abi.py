@@ -72,7 +72,7 @@ def load(path: str = None):
         "moe_vocab_loss_workspace_bytes": ([I64, I, I64, I64, PSZ], I),
         "moe_vocab_loss_fwd": ([P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
         "moe_vocab_loss_bwd": ([P, P, P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
-        "moe_llep_plan": ([P, I, I, I, P, P, P, P, P], I),
+        "moe_llep_plan": ([P, I, I, I, I, P, P, P, P, P], I),
         "moe_llep_dispatch": ([P, P, P, P, P, P, I, I, I64, I, I, I, I64, P, P, P, P, P], I),
         "moe_profile_enable": ([I], I),
         "moe_profile_reset": ([], I),

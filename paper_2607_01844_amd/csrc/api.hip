@@ -487,16 +487,18 @@ MOE_API int moe_vocab_loss_bwd(const moe_bf16* x, const moe_bf16* w_voc, const i
 }
 
 // ------------------------------------------------ least-loaded expert parallelism
-MOE_API int moe_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* win_lo,
-                          int32_t* win_hi, int32_t* load, int32_t* n_ship, void* stream) {
+MOE_API int moe_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int granule,
+                          int32_t* win_lo, int32_t* win_hi, int32_t* load, int32_t* n_ship,
+                          void* stream) {
   const char* fn = "moe_llep_plan";
   CHECK(E >= 1 && E <= MOE_MAX_E, "E out of [1, MOE_MAX_E]");
   CHECK(E_p >= 1 && E_p <= MOE_LLEP_MAX_RANKS, "E_p out of [1, MOE_LLEP_MAX_RANKS]");
   CHECK(E % E_p == 0, "E must be a multiple of E_p");
   CHECK(capacity >= 0, "capacity < 0");
+  CHECK(granule >= 1 && granule <= MOE_LLEP_MAX_GRANULE, "granule out of [1, MOE_LLEP_MAX_GRANULE]");
   REQ(counts); REQ(win_lo); REQ(win_hi); REQ(load); REQ(n_ship);
-  return hip_status(moe::launch_llep_plan(counts, E, E_p, capacity, win_lo, win_hi, load, n_ship,
-                                          static_cast<hipStream_t>(stream)),
+  return hip_status(moe::launch_llep_plan(counts, E, E_p, capacity, granule, win_lo, win_hi, load,
+                                          n_ship, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

@@ -145,8 +145,8 @@ hipError_t launch_permute_noalloc(const uint16_t* x, const int32_t* idx, int64_t
                                   int k, int e_begin, int E_loc, int32_t* offsets,
                                   int32_t* counts_global, int32_t* row_src, int32_t* dst,
                                   uint16_t* x_perm, hipStream_t s);
-hipError_t launch_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* lo,
-                            int32_t* hi, int32_t* load, int32_t* n_ship, hipStream_t s);
+hipError_t launch_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int granule,
+                            int32_t* lo, int32_t* hi, int32_t* load, int32_t* n_ship, hipStream_t s);
 hipError_t launch_llep_dispatch(const uint16_t* x, const int32_t* idx, const int32_t* offsets_all,
                                 const int32_t* dst_all, const int32_t* lo, const int32_t* hi,
                                 int64_t T, int d, int E, int k, int64_t cap, int32_t* offsets_r,

@@ -5,12 +5,17 @@
 // never changes).
 //
 // llep_plan_kernel: one workgroup turns the per-expert assignment counts
-// into per-rank row windows of every expert: each rank keeps its own
-// experts (ascending) up to the capacity C = max(capacity, ceil(L / E_p));
-// the spill of every expert, largest first (ties: lower index), goes in
-// pieces to whichever rank is least loaded (ties: lower rank).  Expert e's
-// assignments, in the layer's stable row order, are cut into consecutive
-// windows: the home rank's first, then the pieces in the order handed out.
+// into per-rank row windows of every expert.  Load is counted in units of g
+// rows (g = 1: rows; g = the grouped GEMM's row-tile height: the tiles a
+// rank's products run, as a window of w rows costs ceil(w / g) of them):
+// each rank keeps its own experts (ascending) up to the capacity
+// C = max(ceil(capacity / g), ceil(U / E_p)) units, U = sum ceil(n_e / g);
+// the spill of every expert, largest first in units (ties: lower index),
+// goes in pieces of whole units to whichever rank has the fewest units
+// (ties: lower rank).  Expert e's assignments, in the layer's stable row
+// order, are cut into consecutive windows: the home rank's first, then the
+// pieces in the order handed out; every window but an expert's last is a
+// whole number of units, so no window splits a tile.
 //
 // llep_window_kernel: one rank's share of an all-expert permutation: the
 // rows of its windows, compacted per expert, and the dst map of the
@@ -25,7 +30,7 @@ namespace {
 constexpr int PT = 1024;  // threads of the plan and offsets kernels
 
 __global__ __launch_bounds__(PT) void llep_plan_kernel(const int32_t* __restrict__ counts, int E,
-                                                       int E_p, int capacity,
+                                                       int E_p, int capacity, int g,
                                                        int32_t* __restrict__ lo,
                                                        int32_t* __restrict__ hi,
                                                        int32_t* __restrict__ load_out,
@@ -33,16 +38,17 @@ __global__ __launch_bounds__(PT) void llep_plan_kernel(const int32_t* __restrict
   __shared__ int n_s[MOE_MAX_E];
   __shared__ int spill_s[MOE_MAX_E];
   __shared__ uint64_t key_s[MOE_MAX_E];
-  __shared__ int load_s[64];
+  __shared__ int load_s[64];   // units
+  __shared__ int rows_s[64];   // rows
   __shared__ int wsum[PT / 64];
   const int tid = threadIdx.x;
   const int G = E / E_p;
 
-  // total assignments and the capacity
+  // total units and the capacity (in units)
   int v = 0;
   for (int e = tid; e < E; e += PT) {
     n_s[e] = counts[e];
-    v += counts[e];
+    v += (counts[e] + g - 1) / g;
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -55,18 +61,22 @@ __global__ __launch_bounds__(PT) void llep_plan_kernel(const int32_t* __restrict
   int total = 0;
 #pragma unroll
   for (int w = 0; w < PT / 64; ++w) total += wsum[w];
-  const int C = max(capacity, (total + E_p - 1) / E_p);
+  const int C = max(capacity / g + (capacity % g != 0), (total + E_p - 1) / E_p);
 
   // keep at home: rank r walks its G experts in ascending order
   if (tid < E_p) {
-    int ld = 0;
+    int ld = 0, rows = 0;
     for (int e = tid * G; e < (tid + 1) * G; ++e) {
-      const int keep = min(n_s[e], C - ld);
-      hi[static_cast<int64_t>(tid) * E + e] = keep;
+      const int u = (n_s[e] + g - 1) / g;
+      const int keep = min(u, C - ld);
+      const int keep_rows = static_cast<int>(min<int64_t>(n_s[e], static_cast<int64_t>(keep) * g));
+      hi[static_cast<int64_t>(tid) * E + e] = keep_rows;
       ld += keep;
-      spill_s[e] = n_s[e] - keep;
+      rows += keep_rows;
+      spill_s[e] = u - keep;
     }
     load_s[tid] = ld;
+    rows_s[tid] = rows;
   }
   __syncthreads();
 
@@ -96,10 +106,11 @@ __global__ __launch_bounds__(PT) void llep_plan_kernel(const int32_t* __restrict
     }
   }
 
-  // hand out the spill, one wave: lane r holds rank r's load
+  // hand out the spill, one wave: lane r holds rank r's load (units, rows)
   if (tid < 64) {
     const int lane = tid;
     int ld = lane < E_p ? load_s[lane] : 0x7fffffff;
+    int rows = lane < E_p ? rows_s[lane] : 0;
     int ships = 0;
     // every piece but the last of an expert fills a rank, so there are at
     // most E + E_p pieces: the bound ends the loop even on inconsistent input
@@ -108,8 +119,8 @@ __global__ __launch_bounds__(PT) void llep_plan_kernel(const int32_t* __restrict
       const uint64_t key = key_s[q];
       if (key == ~0ull) break;
       const int e = static_cast<int>(key & 0xffffffffu);
-      int s = n_s[e] - (0x7fffffff - static_cast<int>(key >> 32));  // first spilled row
-      int left = n_s[e] - s;
+      int left = 0x7fffffff - static_cast<int>(key >> 32);  // spilled units
+      int s = static_cast<int>(static_cast<int64_t>((n_s[e] + g - 1) / g - left) * g);  // first spilled row
       while (left > 0 && budget-- > 0) {
         // least loaded rank, lower rank on ties
         uint64_t best = (static_cast<uint64_t>(static_cast<uint32_t>(ld)) << 32) | static_cast<uint32_t>(lane);
@@ -122,17 +133,21 @@ __global__ __launch_bounds__(PT) void llep_plan_kernel(const int32_t* __restrict
         const int room = C - static_cast<int>(best >> 32);
         const int take = min(left, room);
         if (take <= 0) break;  // no room anywhere: capacity below the total
+        const int nr = static_cast<int>(min<int64_t>(n_s[e] - s, static_cast<int64_t>(take) * g));
         if (lane == 0) {
           lo[static_cast<int64_t>(r) * E + e] = s;
-          hi[static_cast<int64_t>(r) * E + e] = s + take;
+          hi[static_cast<int64_t>(r) * E + e] = s + nr;
         }
-        if (lane == r) ld += take;
-        s += take;
+        if (lane == r) {
+          ld += take;
+          rows += nr;
+        }
+        s += nr;
         left -= take;
         ++ships;
       }
     }
-    if (lane < E_p) load_out[lane] = ld;
+    if (lane < E_p) load_out[lane] = rows;
     if (lane == 0) *n_ship_out = ships;
   }
 }
@@ -188,10 +203,10 @@ __global__ __launch_bounds__(256) void llep_window_kernel(
 
 }  // namespace
 
-hipError_t launch_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int32_t* lo,
-                            int32_t* hi, int32_t* load, int32_t* n_ship, hipStream_t s) {
+hipError_t launch_llep_plan(const int32_t* counts, int E, int E_p, int capacity, int granule,
+                            int32_t* lo, int32_t* hi, int32_t* load, int32_t* n_ship, hipStream_t s) {
   prof_begin(K_LLEP_PLAN, s);
-  llep_plan_kernel<<<1, PT, 0, s>>>(counts, E, E_p, capacity, lo, hi, load, n_ship);
+  llep_plan_kernel<<<1, PT, 0, s>>>(counts, E, E_p, capacity, granule, lo, hi, load, n_ship);
   prof_end(K_LLEP_PLAN, s);
   return hipGetLastError();
 }

@@ -363,10 +363,11 @@ def moe_vocab_loss_bwd(x, w_voc, target, lse, dloss, vblock, dx=None, dw_voc=Non
 
 
 # ------------------------------------------ least-loaded expert parallelism
-def moe_llep_plan(counts, E_p, capacity=0):
-    """Plan of which rank computes which rows of every expert.  counts [E]
-    int32 (device).  Returns (win_lo [E_p,E], win_hi [E_p,E], load [E_p],
-    n_ship [1]), int32 device tensors."""
+def moe_llep_plan(counts, E_p, capacity=0, granule=1):
+    """Plan of which rank computes which rows of every expert, load counted
+    in units of `granule` rows (1: rows; the GEMM row tile, 256: tiles).
+    counts [E] int32 (device).  Returns (win_lo [E_p,E], win_hi [E_p,E],
+    load [E_p] rows, n_ship [1]), int32 device tensors."""
     _need(counts, torch.int32, "counts", 1)
     E = counts.shape[0]
     dev = counts.device
@@ -374,8 +375,8 @@ def moe_llep_plan(counts, E_p, capacity=0):
     hi = torch.empty((E_p, E), dtype=torch.int32, device=dev)
     load = torch.empty((E_p,), dtype=torch.int32, device=dev)
     n_ship = torch.empty((1,), dtype=torch.int32, device=dev)
-    _check(lib.moe_llep_plan(_ptr(counts), E, E_p, capacity, _ptr(lo), _ptr(hi), _ptr(load),
-                             _ptr(n_ship), _stream()), "moe_llep_plan")
+    _check(lib.moe_llep_plan(_ptr(counts), E, E_p, capacity, granule, _ptr(lo), _ptr(hi),
+                             _ptr(load), _ptr(n_ship), _stream()), "moe_llep_plan")
     return lo, hi, load, n_ship
 
 

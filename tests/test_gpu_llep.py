@@ -48,41 +48,46 @@ def _counts_cases():
     return cases
 
 
+@pytest.mark.parametrize("granule", [1, 3, 256])
 @pytest.mark.parametrize("case", _counts_cases(), ids=lambda c: c[0])
-def test_plan_matches_oracle(case):
+def test_plan_matches_oracle(case, granule):
     name, counts, E_p, cap = case
     moe = _moe()
     c = torch.as_tensor(np.asarray(counts, np.int32)).cuda()
-    lo, hi, load, ns = moe.moe_llep_plan(c, E_p, cap)
+    lo, hi, load, ns = moe.moe_llep_plan(c, E_p, cap, granule)
     torch.cuda.synchronize()
-    rlo, rhi, rload, rns = OL.llep_plan(counts, E_p, cap)
+    rlo, rhi, rload, rns = OL.llep_plan(counts, E_p, cap, granule)
     assert np.array_equal(lo.cpu().numpy(), rlo), name
     assert np.array_equal(hi.cpu().numpy(), rhi), name
     assert np.array_equal(load.cpu().numpy(), rload), name
     assert int(ns.item()) == rns, name
-    _say(f"[llep] plan {name}: loads {rload.min()}..{rload.max()} ships {rns}")
+    _say(f"[llep] plan {name} g={granule}: loads {rload.min()}..{rload.max()} ships {rns}")
 
 
-def _plan_and_permute(x, idx, E, E_p, cap_in=0):
+def _plan_and_permute(x, idx, E, E_p, cap_in=0, granule=1):
     moe = _moe()
     pm = moe.moe_permute(x, idx, E, 0, E)
-    lo, hi, load, ns = moe.moe_llep_plan(pm["counts_global"], E_p, cap_in)
+    lo, hi, load, ns = moe.moe_llep_plan(pm["counts_global"], E_p, cap_in, granule)
     return pm, lo, hi, load, ns
 
 
-@pytest.mark.parametrize("T,k,E,E_p,d,s", [(300, 3, 12, 4, 64, 1.5), (1000, 4, 64, 8, 136, 1.2),
-                                           (1, 2, 4, 2, 8, 0.0), (257, 8, 16, 16, 32, 2.0)])
-def test_dispatch_matches_oracle(T, k, E, E_p, d, s):
+@pytest.mark.parametrize("T,k,E,E_p,d,s,granule", [(300, 3, 12, 4, 64, 1.5, 1),
+                                                   (1000, 4, 64, 8, 136, 1.2, 1),
+                                                   (1, 2, 4, 2, 8, 0.0, 1),
+                                                   (257, 8, 16, 16, 32, 2.0, 1),
+                                                   (1000, 4, 64, 8, 136, 1.2, 16),
+                                                   (300, 3, 12, 4, 64, 1.5, 256)])
+def test_dispatch_matches_oracle(T, k, E, E_p, d, s, granule):
     moe = _moe()
     idx_h = W.make_topk(T, k, E, s, seed=T)
     idx = torch.as_tensor(idx_h).cuda()
     g = torch.Generator(device="cpu").manual_seed(1)
     x = torch.randn((T, d), generator=g).to(torch.bfloat16).cuda()
     counts = np.bincount(idx_h.reshape(-1), minlength=E)
-    rlo, rhi, rload, _ = OL.llep_plan(counts, E_p)
-    pm, lo, hi, load, ns = _plan_and_permute(x, idx, E, E_p)
+    rlo, rhi, rload, _ = OL.llep_plan(counts, E_p, 0, granule)
+    pm, lo, hi, load, ns = _plan_and_permute(x, idx, E, E_p, 0, granule)
     assert np.array_equal(lo.cpu().numpy(), rlo) and np.array_equal(hi.cpu().numpy(), rhi)
-    cap = max(int(-(-T * k // E_p)), 1)
+    cap = max(int(rload.max()), 1)
     xb = P.bits(x)
     for r in range(E_p):
         out = moe.moe_llep_dispatch(x, idx, pm["expert_offsets"], pm["dst"], lo, hi, r, cap)
@@ -96,7 +101,7 @@ def test_dispatch_matches_oracle(T, k, E, E_p, d, s):
         dst_ref[rows] = np.arange(n)
         assert np.array_equal(out["dst"].cpu().numpy().reshape(-1), dst_ref)
         assert np.array_equal(P.bits(out["x_perm"])[:n], xb[rows // k])
-    _say(f"[llep] dispatch T={T} k={k} E={E} E_p={E_p}: loads {rload.tolist()}")
+    _say(f"[llep] dispatch T={T} k={k} E={E} E_p={E_p} g={granule}: loads {rload.tolist()}")
 
 
 def _rank_forward(inp, idx, gate, E, E_p, r, pm, lo, hi, cap):
@@ -108,7 +113,7 @@ def _rank_forward(inp, idx, gate, E, E_p, r, pm, lo, hi, cap):
     return out, yp, y
 
 
-def _split_layer(wl, E_p, zipf_s, seed=0):
+def _split_layer(wl, E_p, zipf_s, seed=0, granule=1):
     """Whole-layer forward and its split over E_p ranks; returns both."""
     moe = _moe()
     inp = W.make_inputs(wl, seed=seed, device="cuda")
@@ -116,11 +121,11 @@ def _split_layer(wl, E_p, zipf_s, seed=0):
     idx = torch.as_tensor(idx_h).cuda()
     gate = torch.softmax(torch.randn((wl.T, wl.k), generator=torch.Generator().manual_seed(2)),
                          dim=1).cuda()
-    pm, lo, hi, load, ns = _plan_and_permute(inp["x"], idx, wl.E, E_p)
+    pm, lo, hi, load, ns = _plan_and_permute(inp["x"], idx, wl.E, E_p, 0, granule)
     _, _, yp_all = moe.moe_grouped_swiglu_fwd(pm["x_perm"], pm["expert_offsets"], inp["w_gate"],
                                               inp["w_up"], inp["w_down"])
     y_all = moe.moe_combine(yp_all, pm["dst"], gate)
-    cap = -(-wl.T * wl.k // E_p)
+    cap = max(int(load.max().item()), 1)
     dst_all = pm["dst"].reshape(-1).long()
     y_sum = torch.zeros((wl.T, wl.d), dtype=torch.float32, device="cuda")
     for r in range(E_p):
@@ -148,10 +153,11 @@ def test_split_layer_tiny_against_oracle():
     P.assert_close("whole-layer y", P.f64(y_all), ref_y)
 
 
-@pytest.mark.parametrize("name,E_p,s", [("mid", 8, 1.2), ("large_skew", 8, 1.2)])
-def test_split_layer_full_size(name, E_p, s):
+@pytest.mark.parametrize("name,E_p,s,granule", [("mid", 8, 1.2, 1), ("large_skew", 8, 1.2, 1),
+                                                 ("large_skew", 8, 1.2, 256)])
+def test_split_layer_full_size(name, E_p, s, granule):
     wl = W.WORKLOADS[name]
-    _say(f"[llep] {name} split over {E_p} ranks")
-    _, _, _, y_all, y_sum, load = _split_layer(wl, E_p, s)
+    _say(f"[llep] {name} split over {E_p} ranks, granule {granule}")
+    _, _, _, y_all, y_sum, load = _split_layer(wl, E_p, s, granule=granule)
     _say(f"[llep] {name} loads {load.tolist()}")
     P.assert_close("sum of partial y", P.f64(y_sum), P.f64(y_all))
