@@ -168,8 +168,10 @@ def stored_traffic(workload: str, kernel: str):
 
 
 def chunked_forward(layer, steps: int):
-    """Memory-efficient forward (token chunks on two streams) against the
-    unchunked forward: time per forward and transient buffer bytes."""
+    """Memory-efficient forward against the unchunked forward, time per
+    forward and transient buffer bytes: token chunks (chunks_<n>) and chunks
+    of consecutive permuted rows, i.e. expert ranges (row_chunks_<n>), both
+    on two streams."""
     import ctypes
     m, wl, inp = layer.moe, layer.wl, layer.inp
     dev = inp["x"].device
@@ -209,6 +211,18 @@ def chunked_forward(layer, steps: int):
                                                  wl.expert_begin, wl.E_loc, out=y, stream2=side))
         out[f"chunks_{parts}"] = {"chunk_tokens": chunk, "ms": round(ms, 4),
                                   "transient_bytes": int(n.value)}
+    for parts in (4, 8, 16):
+        rows = -(-cap // parts)
+        n = ctypes.c_size_t()
+        m._check(m.lib.moe_ffn_fwd_row_chunked_workspace_bytes(wl.T, wl.E, wl.k, wl.E_loc, d, f,
+                                                               rows, ctypes.byref(n)),
+                 "moe_ffn_fwd_row_chunked_workspace_bytes")
+        ms = timed(lambda: m.moe_ffn_fwd_row_chunked(inp["x"], layer.idx, layer.gate, wl.E,
+                                                     inp["w_gate"], inp["w_up"], inp["w_down"],
+                                                     rows, wl.expert_begin, wl.E_loc, out=y,
+                                                     stream2=side))
+        out[f"row_chunks_{parts}"] = {"chunk_rows": rows, "ms": round(ms, 4),
+                                      "transient_bytes": int(n.value)}
     return out
 
 
@@ -498,9 +512,10 @@ def layer_stats(layer):
     return int(off[-1]), np.diff(off), int((dst >= 0).any(1).sum())
 
 
-def other_config(name: str, steps: int, warmup: int, flush):
+def other_config(name: str, steps: int, warmup: int, flush, memfwd: bool = False):
     """Step time, GEMM rate and roofline of one more workload (each its own
-    inputs and buffers, freed afterwards)."""
+    inputs and buffers, freed afterwards); with memfwd, its memory-efficient
+    forward too."""
     wl = W.WORKLOADS[name]
     inp = W.make_inputs(wl, seed=0, device="cuda")
     layer = Layer(wl, inp)
@@ -521,6 +536,8 @@ def other_config(name: str, steps: int, warmup: int, flush):
            else round(gemm_tf / PEAK_BF16_TFLOPS, 4),
            "kernels": {k: v for k, v in kernels.items()
                        if "frac_bf16_peak" in v or "frac_hbm_peak" in v}}
+    if memfwd:
+        out["memory_efficient_forward"] = chunked_forward(layer, steps)
     del layer, inp
     torch.cuda.empty_cache()
     return out
@@ -614,7 +631,8 @@ def main():
 
     configs = {}
     for name in [n for n in args.others.split(",") if n and n != wl.name]:
-        configs[name] = other_config(name, args.steps, args.warmup, flush)
+        configs[name] = other_config(name, args.steps, args.warmup, flush,
+                                     memfwd=name == "mid" and not args.no_chunked)
         log(f"[bench] {name}: {configs[name]['ms_per_step']} ms/step, "
             f"GEMMs {configs[name]['grouped_gemm_tflops']} TFLOP/s")
 

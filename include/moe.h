@@ -274,6 +274,36 @@ int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, const float*
                         int64_t chunk, moe_bf16* y, void* workspace, size_t workspace_bytes,
                         void* stream, void* stream2);
 
+/* Expert-range variant of the memory-efficient forward (Sec. 3.3, the same
+ * target as moe_ffn_fwd_chunked).  The whole layer's permutation index
+ * (moe_permute's offsets, row_src and dst, without gathering rows) is formed
+ * once; the permuted rows [0, cap), cap = T * min(k, num_local), are then
+ * taken in chunks of `chunk_rows` consecutive rows (consecutive experts, the
+ * first and last possibly in part).  Each chunk's rows are gathered from x,
+ * pass through moe_grouped_swiglu_fwd, and land in one y_perm of cap rows,
+ * alternating chunks between `stream` and `stream2` with two sets of
+ * buffers; a final moe_combine (weighted by topk_gate) forms y.  Token
+ * chunks read every expert's weights once per chunk; here an expert's
+ * weights are read by the one or two chunks its rows fall in, which is what
+ * a layer bound by its weights needs.  The transient is y_perm (cap x d)
+ * plus two chunks' rows, intermediates and activations, against all cap
+ * rows of x_perm, h_gate, h_up, the activations and y_perm unchunked.  Every
+ * y_perm row depends only on its own token and expert and the combine is
+ * the unchunked one, so y is bit-identical to the unchunked forward.
+ *
+ * Arguments as for moe_ffn_fwd_chunked, with chunk_rows >= 1 in place of
+ * chunk; workspace: moe_ffn_fwd_row_chunked_workspace_bytes(T, ...) bytes
+ * (it grows with T: the index and y_perm cover the whole layer).
+ */
+int moe_ffn_fwd_row_chunked_workspace_bytes(int64_t T, int E, int k, int num_local, int d, int f,
+                                            int64_t chunk_rows, size_t* bytes);
+int moe_ffn_fwd_row_chunked(const moe_bf16* x, const int32_t* topk_idx, const float* topk_gate,
+                            int64_t T, int d, int E, int k, int expert_begin, int num_local,
+                            int f, const moe_bf16* w_gate, const moe_bf16* w_up,
+                            const moe_bf16* w_down, int64_t chunk_rows, moe_bf16* y,
+                            void* workspace, size_t workspace_bytes, void* stream,
+                            void* stream2);
+
 /* ------------------------------------------------------- vocabulary loss
  * Blockwise online loss of the vocabulary projection (Sec. 3.4, eq.
  * (voc-fwd-loss): Y = X W_voc, loss_n = Y[n][t_n] - log sum_v exp Y[n][v]),

@@ -28,6 +28,7 @@ C_SYMBOLS = (
     "moe_grouped_swiglu_workspace_bytes", "moe_grouped_swiglu_fwd", "moe_grouped_swiglu_bwd",
     "moe_combine", "moe_combine_bwd",
     "moe_ffn_fwd_chunked_workspace_bytes", "moe_ffn_fwd_chunked",
+    "moe_ffn_fwd_row_chunked_workspace_bytes", "moe_ffn_fwd_row_chunked",
     "moe_vocab_loss_workspace_bytes", "moe_vocab_loss_fwd", "moe_vocab_loss_bwd",
     "moe_llep_plan", "moe_llep_dispatch",
     "moe_profile_enable", "moe_profile_reset", "moe_profile_num_kernels",
@@ -69,6 +70,9 @@ def load(path: str = None):
         "moe_combine_bwd": ([P, P, P, P, I64, I, I, P, P, P], I),
         "moe_ffn_fwd_chunked_workspace_bytes": ([I64, I, I, I, I, I, PSZ], I),
         "moe_ffn_fwd_chunked": ([P, P, P, I64, I, I, I, I, I, I, P, P, P, I64, P, P, SZ, P, P], I),
+        "moe_ffn_fwd_row_chunked_workspace_bytes": ([I64, I, I, I, I, I, I64, PSZ], I),
+        "moe_ffn_fwd_row_chunked": ([P, P, P, I64, I, I, I, I, I, I, P, P, P, I64, P, P, SZ, P, P],
+                                    I),
         "moe_vocab_loss_workspace_bytes": ([I64, I, I64, I64, PSZ], I),
         "moe_vocab_loss_fwd": ([P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),
         "moe_vocab_loss_bwd": ([P, P, P, P, P, I64, I, I64, I64, P, P, P, SZ, P], I),

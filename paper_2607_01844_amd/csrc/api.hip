@@ -431,6 +431,49 @@ MOE_API int moe_ffn_fwd_chunked(const moe_bf16* x, const int32_t* topk_idx, cons
                     fn);
 }
 
+MOE_API int moe_ffn_fwd_row_chunked_workspace_bytes(int64_t T, int E, int k, int num_local,
+                                                    int d, int f, int64_t chunk_rows,
+                                                    size_t* bytes) {
+  const char* fn = "moe_ffn_fwd_row_chunked_workspace_bytes";
+  CHECK(bytes != nullptr, "bytes is NULL");
+  if (int r = check_tk(fn, T, E, k)) return r;
+  CHECK(num_local >= 1 && num_local <= E, "num_local out of [1, E]");
+  CHECK(chunk_rows >= 1, "chunk_rows < 1");
+  if (int r = check_ffn(fn, num_local, T * std::min(k, num_local), d, f)) return r;
+  *bytes = moe::ffn_fwd_row_chunked_ws_bytes(T, E, k, num_local, d, f, chunk_rows);
+  return MOE_OK;
+}
+
+MOE_API int moe_ffn_fwd_row_chunked(const moe_bf16* x, const int32_t* topk_idx,
+                                    const float* topk_gate, int64_t T, int d, int E, int k,
+                                    int expert_begin, int num_local, int f,
+                                    const moe_bf16* w_gate, const moe_bf16* w_up,
+                                    const moe_bf16* w_down, int64_t chunk_rows, moe_bf16* y,
+                                    void* workspace, size_t workspace_bytes, void* stream,
+                                    void* stream2) {
+  const char* fn = "moe_ffn_fwd_row_chunked";
+  if (int r = check_tk(fn, T, E, k)) return r;
+  CHECK(chunk_rows >= 1, "chunk_rows < 1");
+  CHECK(num_local >= 1 && num_local <= E, "num_local out of [1, E]");
+  CHECK(expert_begin >= 0 && expert_begin + num_local <= E, "expert range out of [0, E)");
+  if (int r = check_ffn(fn, num_local, T * std::min(k, num_local), d, f)) return r;
+  if (T > 0) {
+    REQ(x); REQ(topk_idx); REQ(topk_gate); REQ(y);
+    REQ(w_gate); REQ(w_up); REQ(w_down);
+    const size_t need = moe::ffn_fwd_row_chunked_ws_bytes(T, E, k, num_local, d, f, chunk_rows);
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(MOE_ERR_WORKSPACE, fn,
+                  "workspace smaller than moe_ffn_fwd_row_chunked_workspace_bytes()");
+    OPT(workspace);
+  }
+  return hip_status(moe::launch_ffn_fwd_row_chunked(x, topk_idx, topk_gate, T, d, E, k,
+                                                    expert_begin, num_local, f, w_gate, w_up,
+                                                    w_down, chunk_rows, y, workspace,
+                                                    static_cast<hipStream_t>(stream),
+                                                    static_cast<hipStream_t>(stream2)),
+                    fn);
+}
+
 // ------------------------------------------------------ vocabulary loss
 static int check_vocab(const char* fn, int64_t N, int H, int64_t V, int64_t vblock) {
   CHECK(N >= 0 && N < (int64_t{1} << 31), "N out of [0, 2^31)");

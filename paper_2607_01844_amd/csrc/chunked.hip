@@ -7,6 +7,17 @@
 // other chunk's grouped GEMMs.  Every output row depends only on its own
 // token, so the result is bit-identical to the unchunked forward.
 //
+// The expert-range variant forms the whole layer's permutation index once
+// and walks the permuted rows in chunks of consecutive rows (consecutive
+// experts, the first and last possibly in part): each chunk's rows are
+// gathered, multiplied, and written into one y_perm of all rows, and one
+// combine forms y.  An expert's weights are then read by the one or two
+// chunks its rows fall in, where token chunks read every expert's weights
+// once per chunk; the transient is y_perm plus two chunks' rows,
+// intermediates and activations.  Every y_perm row depends only on its own
+// token and expert and the combine is the unchunked one, so y is again
+// bit-identical to the unchunked forward.
+//
 // Host code only: the kernels are the ones of route/permute/gemm/combine.
 #include <mutex>
 
@@ -121,6 +132,103 @@ hipError_t launch_ffn_fwd_chunked(const uint16_t* x, const int32_t* idx, const f
     if (hipError_t e = stream_after(s0, s1); e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+
+namespace {
+
+struct RowSet {
+  int32_t* offsets;  // [E_loc + 1], relative to the chunk's first row
+  uint16_t* x_perm;  // [rc][d]
+  uint16_t* h_gate;  // [rc][f]
+  uint16_t* h_up;    // [rc][f]
+  void* gemm_ws;
+};
+
+struct RowLayout {
+  int64_t cap, rc;
+  size_t index_bytes, set_bytes;
+};
+
+RowLayout row_layout(int64_t T, int E, int k, int E_loc, int d, int f, int64_t chunk_rows) {
+  RowLayout L;
+  L.cap = T * std::min(k, E_loc);
+  L.rc = std::max<int64_t>(1, std::min(chunk_rows, L.cap));
+  // the whole layer's offsets, row_src, dst, the permutation's workspace and y_perm
+  L.index_bytes = align_up(sizeof(int32_t) * (E_loc + 1), 256) +
+                  align_up(sizeof(int32_t) * static_cast<size_t>(L.cap), 256) +
+                  align_up(sizeof(int32_t) * static_cast<size_t>(T) * k, 256) +
+                  align_up(permute_ws_bytes(T, E, k, E_loc), 256) +
+                  align_up(sizeof(uint16_t) * static_cast<size_t>(L.cap) * d, 256);
+  L.set_bytes = align_up(sizeof(int32_t) * (E_loc + 1), 256) +
+                align_up(sizeof(uint16_t) * static_cast<size_t>(L.rc) * d, 256) +
+                2 * align_up(sizeof(uint16_t) * static_cast<size_t>(L.rc) * f, 256) +
+                align_up(gemm_ws_bytes(L.rc, E_loc, d, f, 0), 256);
+  return L;
+}
+
+}  // namespace
+
+size_t ffn_fwd_row_chunked_ws_bytes(int64_t T, int E, int k, int E_loc, int d, int f,
+                                    int64_t chunk_rows) {
+  const RowLayout L = row_layout(T, E, k, E_loc, d, f, chunk_rows);
+  return L.index_bytes + 2 * L.set_bytes + 256;
+}
+
+hipError_t launch_ffn_fwd_row_chunked(const uint16_t* x, const int32_t* idx, const float* gate,
+                                      int64_t T, int d, int E, int k, int e_begin, int E_loc,
+                                      int f, const uint16_t* wg, const uint16_t* wu,
+                                      const uint16_t* wd, int64_t chunk_rows, uint16_t* y,
+                                      void* ws, hipStream_t s0, hipStream_t s1) {
+  if (T == 0) return hipSuccess;
+  const RowLayout L = row_layout(T, E, k, E_loc, d, f, chunk_rows);
+  char* p = static_cast<char*>(ws);
+  auto take = [&p](size_t bytes) {
+    char* q = p;
+    p += align_up(bytes, 256);
+    return q;
+  };
+  int32_t* offsets = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (E_loc + 1)));
+  int32_t* row_src = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * static_cast<size_t>(L.cap)));
+  int32_t* dst = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * static_cast<size_t>(T) * k));
+  void* perm_ws = take(permute_ws_bytes(T, E, k, E_loc));
+  uint16_t* y_perm = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * static_cast<size_t>(L.cap) * d));
+  RowSet set[2];
+  for (RowSet& b : set) {
+    b.offsets = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (E_loc + 1)));
+    b.x_perm = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * static_cast<size_t>(L.rc) * d));
+    b.h_gate = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * static_cast<size_t>(L.rc) * f));
+    b.h_up = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * static_cast<size_t>(L.rc) * f));
+    b.gemm_ws = take(gemm_ws_bytes(L.rc, E_loc, d, f, 0));
+  }
+  // the whole layer's index (offsets, row_src, dst), without gathering rows
+  if (hipError_t e = launch_permute(x, idx, T, d, E, k, e_begin, E_loc, offsets, nullptr, row_src,
+                                    dst, nullptr, perm_ws, s0);
+      e != hipSuccess)
+    return e;
+  const bool two = s1 != s0;
+  if (two) {  // stream 1 starts after the index (and the caller's work on stream 0)
+    if (hipError_t e = stream_after(s1, s0); e != hipSuccess) return e;
+  }
+  const int64_t nchunks = ceil_div(L.cap, L.rc);
+  for (int64_t c = 0; c < nchunks; ++c) {
+    const int64_t r0 = c * L.rc, rc = std::min(L.rc, L.cap - r0);
+    RowSet& b = set[c & 1];
+    hipStream_t st = (two && (c & 1)) ? s1 : s0;
+    // a buffer set is reused by chunks c and c + 2 on the same stream: in order
+    if (hipError_t e = launch_chunk_rows(x, row_src, offsets, E_loc, r0, rc, d, k, b.offsets,
+                                         b.x_perm, st);
+        e != hipSuccess)
+      return e;
+    if (hipError_t e = launch_ffn_fwd(b.x_perm, b.offsets, E_loc, rc, d, f, wg, wu, wd, b.h_gate,
+                                      b.h_up, y_perm + r0 * d, b.gemm_ws, st);
+        e != hipSuccess)
+      return e;
+  }
+  if (two) {  // every chunk's rows are in y_perm once stream 1's part is done
+    if (hipError_t e = stream_after(s0, s1); e != hipSuccess) return e;
+  }
+  return launch_combine(y_perm, dst, gate, T, d, k, y, s0);
 }
 
 }  // namespace moe

@@ -126,6 +126,13 @@ hipError_t launch_vocab_bwd(const uint16_t* x, const uint16_t* w, const int32_t*
                             const float* lse, const float* dloss, int64_t N, int H, int64_t V,
                             int64_t vblock, uint16_t* dx, uint16_t* dw, void* ws, hipStream_t s);
 size_t ffn_fwd_chunked_ws_bytes(int64_t chunk, int E, int k, int E_loc, int d, int f);
+size_t ffn_fwd_row_chunked_ws_bytes(int64_t T, int E, int k, int E_loc, int d, int f,
+                                    int64_t chunk_rows);
+hipError_t launch_ffn_fwd_row_chunked(const uint16_t* x, const int32_t* idx, const float* gate,
+                                      int64_t T, int d, int E, int k, int e_begin, int E_loc,
+                                      int f, const uint16_t* wg, const uint16_t* wu,
+                                      const uint16_t* wd, int64_t chunk_rows, uint16_t* y,
+                                      void* ws, hipStream_t s0, hipStream_t s1);
 hipError_t launch_ffn_fwd_chunked(const uint16_t* x, const int32_t* idx, const float* gate,
                                   int64_t T, int d, int E, int k, int e_begin, int E_loc, int f,
                                   const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
@@ -138,6 +145,12 @@ hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int 
                           hipStream_t s);
 hipError_t launch_gather(const uint16_t* x, const int32_t* dst, int64_t T, int d, int k,
                          uint16_t* x_perm, hipStream_t s);
+// Rows [r0, r0 + rc) of a permutation (offsets, row_src over all local
+// experts) as a chunk: offsets_c [E_loc + 1] relative to r0 and clamped to
+// [0, rc], and x_perm_c [rc][d] (its filled rows) gathered from x.
+hipError_t launch_chunk_rows(const uint16_t* x, const int32_t* row_src, const int32_t* offsets,
+                             int E_loc, int64_t r0, int64_t rc, int d, int k, int32_t* offsets_c,
+                             uint16_t* x_perm_c, hipStream_t s);
 // launch_permute with the library's static scratch as the workspace
 // (permute_ws_bytes(T, E, k, E_loc) <= MOE_PERMUTE_NOALLOC_MAX_BYTES, checked
 // by the caller)

@@ -234,6 +234,33 @@ __global__ __launch_bounds__(256) void perm_gather_kernel(const uint16_t* __rest
   }
 }
 
+// Rows [r0, r0 + rc) of the permuted order (consecutive experts, the first
+// and last possibly in part) as a layer of their own: their expert offsets,
+// offsets_c[e] = clamp(offsets[e] - r0, 0, rc) for e = 0..E_loc, and their
+// rows of x (row i from token row_src[r0 + i] / k), up to the last filled
+// row.  One wave per row, 16 bytes per lane.
+__global__ __launch_bounds__(256) void perm_chunk_rows_kernel(
+    const uint16_t* __restrict__ x, const int32_t* __restrict__ row_src,
+    const int32_t* __restrict__ offsets, int E_loc, int64_t r0, int64_t rc, int d, int k,
+    int32_t* __restrict__ offsets_c, uint16_t* __restrict__ x_perm_c) {
+  auto clamp_rows = [&](int32_t o) {
+    return static_cast<int32_t>(min(max(static_cast<int64_t>(o) - r0, int64_t{0}), rc));
+  };
+  if (blockIdx.x == 0) {
+    for (int e = threadIdx.x; e <= E_loc; e += blockDim.x) offsets_c[e] = clamp_rows(offsets[e]);
+  }
+  const int64_t m = clamp_rows(offsets[E_loc]);
+  const int lane = threadIdx.x & 63;
+  const int nch = d >> 3;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); i < m;
+       i += static_cast<int64_t>(gridDim.x) * 4) {
+    const int64_t t = row_src[r0 + i] / k;
+    const uint4* src = reinterpret_cast<const uint4*>(x + t * d);
+    uint4* out = reinterpret_cast<uint4*>(x_perm_c + i * d);
+    for (int c = lane; c < nch; c += 64) out[c] = src[c];
+  }
+}
+
 struct PermWs {
   int32_t* blk_loc;
   int32_t* blk_glob;
@@ -286,9 +313,21 @@ hipError_t launch_permute(const uint16_t* x, const int32_t* idx, int64_t T, int 
                                                                      nbits, w.pre, row_src, dst);
   prof_end(K_PERM_RANK, s);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  if (x_perm == nullptr) return hipSuccess;  // the index only
   prof_begin(K_PERM_GATHER, s);
   perm_gather_kernel<<<static_cast<unsigned>(ceil_div(T, 4)), 256, 0, s>>>(x, dst, T, d, k,
                                                                            x_perm);
+  prof_end(K_PERM_GATHER, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_rows(const uint16_t* x, const int32_t* row_src, const int32_t* offsets,
+                             int E_loc, int64_t r0, int64_t rc, int d, int k, int32_t* offsets_c,
+                             uint16_t* x_perm_c, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>(ceil_div(rc, 4), 1 << 16)));
+  prof_begin(K_PERM_GATHER, s);
+  perm_chunk_rows_kernel<<<grid, 256, 0, s>>>(x, row_src, offsets, E_loc, r0, rc, d, k, offsets_c,
+                                              x_perm_c);
   prof_end(K_PERM_GATHER, s);
   return hipGetLastError();
 }

@@ -314,6 +314,35 @@ def moe_ffn_fwd_chunked(x, topk_idx, topk_gate, E, w_gate, w_up, w_down, chunk, 
     return out
 
 
+def moe_ffn_fwd_row_chunked(x, topk_idx, topk_gate, E, w_gate, w_up, w_down, chunk_rows,
+                            expert_begin=0, num_local=None, out=None, stream2=None):
+    """Memory-efficient forward over chunks of consecutive permuted rows
+    (expert ranges) on the current stream and `stream2` (a torch.cuda.Stream
+    or None = the current stream).  Returns y."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(topk_idx, torch.int32, "topk_idx", 2)
+    _need(topk_gate, torch.float32, "topk_gate", 2)
+    for n, w in (("w_gate", w_gate), ("w_up", w_up), ("w_down", w_down)):
+        _need(w, torch.bfloat16, n, 3)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    num_local = w_gate.shape[0] if num_local is None else num_local
+    f = w_gate.shape[2]
+    if out is None:
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=x.device)
+    n = ctypes.c_size_t()
+    _check(lib.moe_ffn_fwd_row_chunked_workspace_bytes(T, E, k, num_local, d, f, chunk_rows,
+                                                       ctypes.byref(n)),
+           "moe_ffn_fwd_row_chunked_workspace_bytes")
+    ws = workspace(n.value, x.device, "ffn_fwd_row_chunked")
+    s2 = _stream() if stream2 is None else ctypes.c_void_p(stream2.cuda_stream)
+    _check(lib.moe_ffn_fwd_row_chunked(_ptr(x), _ptr(topk_idx), _ptr(topk_gate), T, d, E, k,
+                                       expert_begin, num_local, f, _ptr(w_gate), _ptr(w_up),
+                                       _ptr(w_down), chunk_rows, _ptr(out), _ptr(ws), ws.numel(),
+                                       _stream(), s2), "moe_ffn_fwd_row_chunked")
+    return out
+
+
 # ------------------------------------------------------- vocabulary loss
 def _vocab_ws(N, H, V, vblock, device):
     n = ctypes.c_size_t()

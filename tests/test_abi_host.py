@@ -135,3 +135,24 @@ def test_chunked_workspace_depends_on_chunk_only(lib):
     per_set = rows * (2 * 2048 + 3 * 1408) * 2  # x_perm, y_perm, h_gate, h_up, act
     assert n1.value >= 2 * per_set
     assert 1.9 < n2.value / n1.value < 2.1
+
+
+def test_row_chunked_workspace_layout(lib):
+    """The expert-range forward keeps the whole layer's index and y_perm plus
+    two chunks' rows, intermediates and activations: at mid sizes with four
+    chunks it stays below two thirds of the unchunked transient, and halving
+    the chunk takes away about half of the chunk part."""
+    T, E, k, d, f = 4096, 64, 6, 2048, 1408
+    cap = T * k
+    full = cap * (2 * d + 3 * f) * 2  # x_perm, y_perm, h_gate, h_up, act
+    n4, n8 = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.moe_ffn_fwd_row_chunked_workspace_bytes(T, E, k, E, d, f, cap // 4,
+                                                       ctypes.byref(n4)) == 0
+    assert lib.moe_ffn_fwd_row_chunked_workspace_bytes(T, E, k, E, d, f, cap // 8,
+                                                       ctypes.byref(n8)) == 0
+    fixed = cap * d * 2 + cap * 4 + T * k * 4  # y_perm, row_src, dst
+    per_chunk_row = (d + 3 * f) * 2  # x_perm, h_gate, h_up, act of one row
+    assert n4.value >= fixed + 2 * (cap // 4) * per_chunk_row
+    assert n4.value < 0.65 * full
+    assert n8.value < 0.45 * full
+    assert abs((n4.value - fixed) / (n8.value - fixed) - 2) < 0.05
