@@ -1181,10 +1181,10 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
       // A finished tile leaves in four passes, one per 32-row block i of
       // every wave's 128 x 64 accumulator block: each wave writes its block i
       // as bf16 into its 4 KiB patch of a pass slot (wave X at X * 4 KiB),
-      // and after the barrier each wave of group 1 reads two patches (of wave
-      // q of group 0 and its own) and stores them.  The patch layouts carry
-      // XOR swizzles that keep the 64 banks conflict-free (bf16 rows 16..31
-      // hold their two 8-byte halves swapped).
+      // and after the barrier the four waves of group 1 each store a quarter
+      // of the pass as 256-byte row pieces.  The patch layouts carry XOR
+      // swizzles that keep the 64 banks conflict-free (bf16 rows 16..31 hold
+      // their two 8-byte halves swapped).
       typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
       typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
       auto unswap = [](uint4 v, int r) __attribute__((always_inline)) {
@@ -1219,43 +1219,51 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
           });
         }
       };
-      // block i of wave X's accumulators (tile tl), from its patch to memory
-      auto store_block = [&](const Tile& tl, auto IC, const lds_char* patch, int X) __attribute__((always_inline)) {
+      // Pass i's rows (block i of every wave's accumulators, in slot S) to
+      // memory, one quarter per wave q of group 1, as rows of 256 bytes:
+      // dual, the row half wm = q % 2 of output q / 2 (gate, up) across the
+      // four column groups; otherwise the row half wm and column groups
+      // 2 (q / 2) and 2 (q / 2) + 1.  Each store instruction covers 4 rows;
+      // each group of 16 lanes reads 256 consecutive patch bytes.
+      auto store_pass = [&](const Tile& tl, auto IC, const lds_char* S) __attribute__((always_inline)) {
         constexpr int i = IC;
         const int e = tl.e, m0 = tl.m0, n0 = tl.n0;
         const int ln = opaque(threadIdx.x & 63);
         const int mvalid = DENSE ? (g.dM - m0) : ((MODE == WGRAD_GATE_UP ? d : f) - m0);
-        const int rb = (X & 1) * 128 + 32 * i;  // tile row of the block's first row
-        const int xn = X >> 1;                  // the producing wave's column group
+        const int qm = w & 1, qh = (w >> 1) & 1;  // this wave's quarter (group 1)
+        const int rb = qm * 128 + 32 * i;  // tile row of the block's first row
         if (rb >= mvalid) return;
-        auto get16 = [&](int off) __attribute__((always_inline)) {
+        auto get16 = [&](const lds_char* patch, int off) __attribute__((always_inline)) {
           const u32x4v v = *(const __attribute__((address_space(3))) u32x4v*)(patch + off);
           return make_uint4(v[0], v[1], v[2], v[3]);
         };
         if constexpr (DUAL) {
-          static_for<2>([&](auto Tt) {
+          const int xn = ln >> 4, rr = (ln >> 2) & 3, c = ln & 3;
+          const lds_char* patch = S + (qm + 2 * xn) * PATCH_BYTES + qh * 2048;
+          uint16_t* const out = (qh ? g.dwu : g.dwg) + e * wdf;
+          const int col = n0 + xn * 32 + 8 * c;
+          static_for<8>([&](auto Tt) {
             constexpr int t = Tt;
-            const int r = 16 * t + (ln >> 2), c = ln & 3;
-            const int off = r * 64 + ((c ^ ((r >> 2) & 3)) << 4);
-            const uint4 hgv = unswap(get16(off), r), huv = unswap(get16(2048 + off), r);
-            const int rt = rb + r, col = n0 + xn * 32 + 8 * c;
-            if (rt < mvalid && col < f) {
-              const int64_t o = e * wdf + (int64_t)(m0 + rt) * f + col;
-              *reinterpret_cast<uint4*>(g.dwg + o) = hgv;
-              *reinterpret_cast<uint4*>(g.dwu + o) = huv;
-            }
+            const int r = 4 * t + rr;
+            const uint4 v = unswap(get16(patch, r * 64 + ((c ^ (t & 3)) << 4)), r);
+            const int rt = rb + r;
+            if (rt < mvalid && col < f)
+              *reinterpret_cast<uint4*>(out + (int64_t)(m0 + rt) * f + col) = v;
           });
         } else {
-          static_for<4>([&](auto Tt) {
+          const int xn = 2 * qh + (ln >> 5), rr = (ln >> 3) & 3, c = ln & 7;
+          const lds_char* patch = S + (qm + 2 * xn) * PATCH_BYTES;
+          const int col = n0 + xn * 64 + 8 * c;
+          static_for<8>([&](auto Tt) {
             constexpr int t = Tt;
-            const int r = 8 * t + (ln >> 3), c = ln & 7;
-            const uint4 v = unswap(get16(r * 128 + ((c ^ ((r >> 1) & 7)) << 4)), r);
-            const int rt = rb + r, col = n0 + xn * 64 + 8 * c;
+            const int r = 4 * t + rr;
+            const uint4 v = unswap(get16(patch, r * 128 + ((c ^ ((r >> 1) & 7)) << 4)), r);
+            const int rt = rb + r;
             if (rt < mvalid && col < (DENSE ? g.dN : d)) {
-              uint16_t* out;
-              if constexpr (MODE == WGRAD_DOWN) out = g.dwd + e * wdf + (int64_t)(m0 + rt) * d;
-              else out = static_cast<uint16_t*>(g.dc) + (int64_t)(m0 + rt) * g.c_ld + g.cc0;  // VOC_DW
-              *reinterpret_cast<uint4*>(out + col) = v;
+              uint16_t* o;
+              if constexpr (MODE == WGRAD_DOWN) o = g.dwd + e * wdf + (int64_t)(m0 + rt) * d;
+              else o = static_cast<uint16_t*>(g.dc) + (int64_t)(m0 + rt) * g.c_ld + g.cc0;  // VOC_DW
+              *reinterpret_cast<uint4*>(o + col) = v;
             }
           });
         }
@@ -1336,17 +1344,13 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
             static_for<4>([&](auto P) {
               constexpr int p = P;
               put_block(P, (p & 1 ? S1 : S0) + w * PATCH_BYTES);
-              if constexpr (G == 1 && p > 0) {
-                lds_char* const Sp = (p - 1) & 1 ? S1 : S0;
-                store_block(tp, std::integral_constant<int, p - 1>{}, Sp + wq * PATCH_BYTES, wq);
-                store_block(tp, std::integral_constant<int, p - 1>{}, Sp + w * PATCH_BYTES, w);
-              }
+              if constexpr (G == 1 && p > 0)
+                store_pass(tp, std::integral_constant<int, p - 1>{}, (p - 1) & 1 ? S1 : S0);
               phase_end();
             });
             zero_acc();
             if constexpr (G == 1) {
-              store_block(tp, std::integral_constant<int, 3>{}, S1 + wq * PATCH_BYTES, wq);
-              store_block(tp, std::integral_constant<int, 3>{}, S1 + w * PATCH_BYTES, w);
+              store_pass(tp, std::integral_constant<int, 3>{}, S1);
               if (tc.valid) phase_end();
             }
           }
