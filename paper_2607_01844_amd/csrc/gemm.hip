@@ -1704,7 +1704,11 @@ __global__ __launch_bounds__(NTHR, 1) void grouped_gemm_kernel(GemmArgs g) {
         epilogue(tc, patch);
         zero_acc();
         // the patch reads are done once the LDS counter drains; the stores stay
-        // in flight (the next sync's vector-memory wait covers them, in order)
+        // in flight.  The next sync's vector-memory wait covers them: the
+        // operations it may leave in flight are B's refill loads below, issued
+        // after them (stores and loads share that counter but need not
+        // complete in order relative to each other, so a wait may only leave
+        // loads in flight that were issued after everything it must cover).
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();  // every wave is done with its patch
         __builtin_amdgcn_sched_barrier(0);
