@@ -4,11 +4,11 @@ share of the layer under that plan.
 TEST INFRASTRUCTURE ONLY: imported by tests/ and the benchmark, never by the
 product path.  It shares no code with the HIP library.
 
-Mixture-of-Parallelisms Sec. 3.3 (recap of LLEP): at every MoE call the
-per-rank token load is measured, excess tokens move from overloaded ranks
-to underloaded ones, and the expert weights travel with them so that the
-receiving rank computes those token-expert products itself; which products
-are computed never changes.  The paper gives no planning steps (they are in
+Mixture-of-Parallelisms Sec. 3.3 (recap of LLEP): each call measures how
+much work every rank holds; a rank above its share hands part of it, with
+the weights of the experts concerned, to ranks below their share, which
+then compute those token-expert products themselves; the set of products
+computed stays the same.  The paper gives no planning steps (they are in
 the LLEP paper, which is not available), so the plan below is a reading of
 that description, fully specified so that the device planner can be checked
 bit for bit:

@@ -1,8 +1,8 @@
 // Least-loaded expert parallelism on the device (Mixture-of-Parallelisms
-// Sec. 3.3, recap of LLEP: per-rank load is measured at every MoE call,
-// excess token-expert assignments move from overloaded to underloaded ranks
-// and the expert weights travel with them; which products are computed
-// never changes).
+// Sec. 3.3, recap of LLEP: each call measures the work every rank holds; a
+// rank above its share hands part of it, with the weights of the experts
+// concerned, to ranks below their share; the set of products computed stays
+// the same).
 //
 // llep_plan_kernel: one workgroup turns the per-expert assignment counts
 // into per-rank row windows of every expert.  Load is counted in units of g
