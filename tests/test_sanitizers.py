@@ -129,6 +129,8 @@ for T in (0, 1, 4096, 1 << 31, B):
     L.moe_permute_workspace_bytes(T, 1024, 16, 1024, ctypes.byref(n))
     L.moe_grouped_swiglu_workspace_bytes(T, 1024, 262144, 262144, 3, ctypes.byref(n))
     L.moe_ffn_fwd_chunked_workspace_bytes(T, 262144, 1024, 16, 1024, 262144, ctypes.byref(n))
+    L.moe_ffn_fwd_row_chunked_workspace_bytes(T, 1024, 16, 1024, 262144, 262144, B, ctypes.byref(n))
+    L.moe_ffn_fwd_row_chunked_workspace_bytes(T, 64, 6, 64, 2048, 1408, 1, ctypes.byref(n))
     L.moe_vocab_loss_workspace_bytes(T, 262144, B, 1 << 32, ctypes.byref(n))
     L.moe_vocab_loss_workspace_bytes(T, 8, 9, 8, ctypes.byref(n))
 print("CHILD OK")
