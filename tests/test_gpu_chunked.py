@@ -138,7 +138,7 @@ def test_row_chunked_forward_matches_oracle():
     P.assert_close("y (row-chunked)", P.f64(ref), o["y"])
 
 
-@pytest.mark.parametrize("name", ["mid", "ep_share"])
+@pytest.mark.parametrize("name", ["mid", "ep_share", "long"])
 def test_row_chunked_forward_full_size(name):
     wl = W.WORKLOADS[name]
     cap = wl.T * min(wl.k, wl.E_loc)
