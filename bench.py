@@ -351,6 +351,40 @@ def llep_leg(steps: int, E_p: int = 8, name: str = "large_skew", granule: int = 
             "row_balanced_plan": leg(1)}
 
 
+def graph_replay(names, steps: int):
+    """One whole layer step (route through the permutation backward, via
+    layer_fwd_bwd) timed eagerly and as one captured HIP graph, for the small
+    workloads where launch overhead shows: milliseconds per step each."""
+    from paper_2607_01844_amd import moe
+    out = {}
+    for name in names:
+        wl = W.WORKLOADS[name]
+        inp = W.make_inputs(wl, seed=5, device="cuda")
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):  # sizes the cached workspaces before capture
+            moe.layer_fwd_bwd(inp, wl.k, keep=False)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            moe.layer_fwd_bwd(inp, wl.k, keep=False)
+        res = {}
+        for label, fn in (("eager_ms", lambda: moe.layer_fwd_bwd(inp, wl.k, keep=False)),
+                          ("graph_ms", g.replay)):
+            fn()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                fn()
+            torch.cuda.synchronize()
+            res[label] = round((time.perf_counter() - t0) / steps * 1e3, 4)
+        out[name] = res
+        del g, inp
+        torch.cuda.empty_cache()
+    return out
+
+
 def vocab_loss(steps: int, warmup: int):
     """Blockwise vocabulary loss on its own workload (Sec. 3.4): forward,
     backward and both, with the dense-equivalent FLOP rate (2NHV forward,
@@ -561,6 +595,8 @@ def main():
                     help="skip the vendor batched-GEMM context measurement")
     ap.add_argument("--no-chunked", action="store_true",
                     help="skip the memory-efficient forward leg")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the captured-graph leg (tiny and mid steps replayed)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
@@ -642,6 +678,11 @@ def main():
         log(f"[bench] least-loaded expert parallelism: {llep}")
         torch.cuda.empty_cache()
 
+    graph = None
+    if not args.no_graph:
+        graph = graph_replay(["tiny", "mid"], args.steps)
+        log(f"[bench] captured-graph steps: {graph}")
+
     voc = None
     if not args.no_vocab:
         voc = vocab_loss(args.steps, args.warmup)
@@ -674,6 +715,7 @@ def main():
         "memory_efficient_forward": memfwd,
         "llep": llep,
         "vocab_loss": voc,
+        "graph_replay": graph,
         "vendor_batched_gemm_context": vendor,
         "device": torch.cuda.get_device_name(0),
     }
